@@ -1,0 +1,197 @@
+/*
+ * fsched — batched evaluation of resource-fair LLM batching on AMD Instinct
+ * MI355X (gfx950).  C ABI of libfsched.so.
+ *
+ * The library evaluates many independent instances of the scheduling model of
+ * "Efficiency and Cost Alignment in Batched LLM Serving via Resource-Fair
+ * Scheduling" (Yao & Zhou):
+ *   - Section 2: n requests, request i processes prompt_i + output_i tokens one
+ *     per step (chunked prefill: the paper's o_i counts prompt and output
+ *     tokens); at most B requests run per step; the fairness constraint,
+ *     eq. (1), bounds the spread of the progress a_i(t) of co-running requests
+ *     by alpha;
+ *   - Section 3: the policies LJF (Algorithm 1) and ISJL (Algorithm 2 for B = 2,
+ *     Algorithm 3 for B >= 2), run on the released queue (Section 3.5,
+ *     Online-ISJL), plus the unfair baselines FCFS and SJF of Section 2.1;
+ *   - Section 5: the cost of step t is c + tau |S_t| max_{S_t} r_i with
+ *     r_i = a_i + 1, and Theorem 5.1 splits the total into tau Q + c T + tau E.
+ * In addition to the paper's model every call takes a KV budget M_kv: the
+ * reservations (full lengths) of co-running requests must fit in M_kv unless a
+ * request runs alone.
+ *
+ * Conventions shared by every call
+ *   - Job tables are row-major [n_inst][n_jobs] int32: arrival step (>= 0),
+ *     prompt tokens (>= 0) and output tokens (>= 1) of every job.
+ *   - Steps are 0-based.  A job started at step s is active on steps
+ *     s .. s + len - 1 (len = prompt + output) and completes at s + len; the
+ *     makespan T is the latest completion, idle steps included.
+ *   - Pointers: with FSCHED_F_DEVICE_PTRS every array argument is a device
+ *     pointer and the call only enqueues work on `stream` (a hipStream_t, or
+ *     NULL for the null stream); outputs are valid once the stream reaches the
+ *     call.  Without the flag every array is host memory; the library stages
+ *     through device memory it allocates and frees itself and returns after
+ *     the results are back in host memory.
+ *   - The caller owns every buffer.  The library keeps no pointer after the
+ *     call (host mode) or after the stream passes the call (device mode).
+ *   - Return codes are FSCHED_OK or a negative FSCHED_E* code; outputs are
+ *     undefined on error.  Argument errors (null pointers, bad sizes or
+ *     parameters) are detected before any work is enqueued.  In device mode the
+ *     job tables are not read on the host: an instance whose table is invalid
+ *     (or exceeds a kernel limit) gets T = FSCHED_T_INVALID / FSCHED_T_RANGE /
+ *     FSCHED_T_TOOLARGE in its metrics and every other field zero; host mode
+ *     checks the tables first and returns the matching error code instead.
+ *   - Kernel limits: n_jobs <= 4096; min(B, n_jobs) <= 1024; len < 2^20; when
+ *     the arrivals of an instance are not non-decreasing in job index, every
+ *     arrival < 2^20.  Beyond them: FSCHED_ETOOLARGE / FSCHED_T_TOOLARGE.
+ */
+#ifndef FSCHED_H
+#define FSCHED_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FSCHED_ABI_VERSION 1
+
+#define FSCHED_ALPHA_INF INT32_MAX /* fairness budget = infinity             */
+#define FSCHED_UNLIMITED 0         /* B = 0: no count limit; M_kv = 0: none   */
+
+enum { FSCHED_FCFS = 0, FSCHED_LJF = 1, FSCHED_ISJL = 2, FSCHED_SJF = 3 };
+
+enum {
+  FSCHED_OK = 0,
+  FSCHED_EINVAL = -1,    /* bad argument or job table                        */
+  FSCHED_ERANGE = -2,    /* an int64 accumulator could overflow              */
+  FSCHED_ENOMEM = -3,    /* device or host allocation failed                 */
+  FSCHED_EDEVICE = -4,   /* a HIP call failed (see fsched_last_hip_error)     */
+  FSCHED_ETOOLARGE = -5, /* beyond a kernel limit                            */
+  FSCHED_ENOTIMPL = -6,
+  FSCHED_EINTERNAL = -7  /* the event loop of an instance found no next event */
+};
+
+/* Per-instance markers written into fsched_metrics.T in device mode. */
+#define FSCHED_T_INVALID (-1)
+#define FSCHED_T_RANGE (-2)
+#define FSCHED_T_TOOLARGE (-5)
+#define FSCHED_T_INTERNAL (-7)
+
+enum {
+  FSCHED_F_DEVICE_PTRS = 1u, /* array arguments are device pointers            */
+  FSCHED_F_SYNC = 4u,        /* device mode: synchronize the stream before return */
+  FSCHED_F_BETA_SQRT17 = 8u  /* ISJL: beta = floor((sqrt(17)-1) alpha / 4), the
+                                B = 2 choice of Section 3.2; default beta = alpha
+                                (Section 3.3)                                   */
+};
+
+/* Scheduling and cost parameters (40 bytes, no padding). */
+typedef struct {
+  int32_t B;        /* max requests per step (paper's B), >= 1, or FSCHED_UNLIMITED */
+  int32_t alpha;    /* fairness budget on progress, >= 0, or FSCHED_ALPHA_INF        */
+  int64_t M_kv;     /* KV reservation budget in tokens, >= 1, or FSCHED_UNLIMITED    */
+  int32_t policy;   /* FSCHED_FCFS | FSCHED_LJF | FSCHED_ISJL | FSCHED_SJF           */
+  uint32_t flags;   /* FSCHED_F_*                                                    */
+  int64_t cost_c;   /* fixed cost of one step, c >= 0 (integer units)                */
+  int64_t cost_tau; /* footprint coefficient tau >= 0 (integer units)                */
+} fsched_params;
+
+/* Per-instance results (104 bytes); every field is exact.
+ *   T               makespan (steps, idle steps included)
+ *   O               sum of lengths (tokens)
+ *   Q               intrinsic term sum_i len_i (len_i + 1) / 2        (Thm 5.1)
+ *   E               batching externality sum_t sum_S (max r - r_i)     (Thm 5.1)
+ *   C               total cost sum_t (c + tau |S_t| max r); equals c T + tau (Q + E)
+ *   W               max-driven step cost sum_t (c + tau max r) (no |S| factor)
+ *   sum_completion  sum_i (s_i + len_i)
+ *   sum_latency     sum_i (s_i + len_i - arrival_i)
+ *   sum_extent      sum over busy steps of (max r - min r)
+ *   busy_steps      steps with at least one active job
+ *   peak_kv         max over steps of sum_S r_i (tokens held)
+ *   unfair_steps    steps whose extent exceeds alpha
+ *   max_extent      max over steps of the extent
+ *   max_active      max over steps of |S_t|                                     */
+typedef struct {
+  int64_t T, O, Q, E, C, W;
+  int64_t sum_completion, sum_latency;
+  int64_t sum_extent, busy_steps;
+  int64_t peak_kv, unfair_steps;
+  int32_t max_extent, max_active;
+} fsched_metrics;
+
+/* fsched_simulate — run every instance under p->policy and report its metrics.
+ *
+ * Policies (Sections 2.1 and 3):
+ *   FCFS  continuous batching in (arrival, index) order; admission stops at the
+ *         first released job that does not fit B or M_kv; no fairness guard.
+ *   SJF   the same in (length, index) order.
+ *   LJF   Algorithm 1: at an empty machine start the longest released jobs, at
+ *         most B and stopping at the first that does not fit M_kv; admit nothing
+ *         else until the machine is empty again.
+ *   ISJL  Algorithms 2/3 on the released queue: Phase ONE builds a plan around
+ *         the longest job (short-job packs under the caps min{2 alpha,
+ *         o_1 - o_j + beta}, spare workers with packs up to alpha, worker 1
+ *         delayed by min{max{max pack - alpha, 0}, alpha}); every plan start and
+ *         every Phase TWO admission is guarded by A_max(t) <= alpha; when Phase
+ *         TWO finds A_max(t) > alpha it drains until the machine is empty and
+ *         Phase ONE runs again.  The plan uses at most as many workers as the
+ *         longest queued jobs can fill within M_kv.
+ *
+ * Arguments
+ *   p        parameters (host pointer, read during the call).
+ *   n_inst   number of instances, >= 0 (0: nothing is done).
+ *   n_jobs   jobs per instance, >= 1.
+ *   arrival, prompt, output   job tables [n_inst][n_jobs].
+ *   out      [n_inst] metrics.
+ *   start, finish   nullable [n_inst][n_jobs] int32: start step and completion
+ *            step of every job.
+ *   stream   hipStream_t (device mode) or NULL.
+ * Errors: EINVAL (null required pointer, n_jobs < 1, n_inst < 0, B < 0,
+ *   alpha < 0, M_kv < 0, cost < 0, unknown policy or flag, invalid table in host
+ *   mode), ERANGE (host mode: an accumulator could exceed int64), ETOOLARGE,
+ *   ENOMEM, EDEVICE. */
+int fsched_simulate(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
+                    const int32_t* arrival, const int32_t* prompt, const int32_t* output,
+                    fsched_metrics* out, int32_t* start, int32_t* finish, void* stream);
+
+/* fsched_cost_decompose — re-score given schedules (start steps) from the
+ * schedule alone (Section 5 terms as in fsched_metrics) and check them.
+ *   start      [n_inst][n_jobs] int32 start steps.
+ *   violation  [n_inst] uint32 bit mask: 1 a start before its arrival;
+ *              2 more than B jobs active at some step; 4 reservations above
+ *              M_kv with two or more jobs active; 8 progress range above alpha
+ *              (eq. (1)); 16 a negative start (metrics are zero then).
+ * p->policy and p->flags other than DEVICE_PTRS / SYNC are ignored.
+ * Errors as fsched_simulate. */
+int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
+                          const int32_t* arrival, const int32_t* prompt,
+                          const int32_t* output, const int32_t* start, fsched_metrics* out,
+                          uint32_t* violation, void* stream);
+
+/* fsched_bruteforce_opt — exact alpha-fair optimum makespan (Appendix A's
+ * integer program with release steps and M_kv added): the least makespan over
+ * every start vector with s_i >= arrival_i, at most B active jobs per step,
+ * reservations within M_kv unless a job runs alone, and |s_i - s_j| <= alpha for
+ * every pair active at a common step.
+ *   n_jobs     <= 8 (ETOOLARGE otherwise); every length <= 255.
+ *   T_opt      [n_inst] int64 optimum makespan.
+ *   start_opt  nullable [n_inst][n_jobs] int32: one optimal schedule.
+ * p->policy, cost_c and cost_tau are ignored. */
+int fsched_bruteforce_opt(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
+                          const int32_t* arrival, const int32_t* prompt, const int32_t* output,
+                          int64_t* T_opt, int32_t* start_opt, void* stream);
+
+/* Text for a return code (static storage). */
+const char* fsched_strerror(int code);
+
+/* FSCHED_ABI_VERSION of the loaded library. */
+int fsched_abi_version(void);
+
+/* The hipError_t of the last FSCHED_EDEVICE return on the calling thread. */
+int fsched_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FSCHED_H */

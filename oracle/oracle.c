@@ -282,18 +282,29 @@ static void phase_one(or_sim* S, const int32_t* ord_long, int64_t t, uint32_t fl
   if (k == 0) return;
   S->mode = 0; /* FILL */
   const int64_t a = I->alpha;
+  /* Reading (the paper has no KV budget): the plan uses only as many workers as
+   * the longest queued jobs can occupy together, Bp = the largest k <= B whose k
+   * longest jobs' reservations fit M_kv (at least one).  At alpha = 0 this keeps
+   * ISJL identical to LJF. */
+  int64_t Bp = 0, resv = 0;
+  for (int32_t q = 0; q < k && Bp < I->B; ++q) {
+    int64_t L = I->len[S->pool[q]];
+    if (I->M != 0 && q > 0 && resv + L > I->M) break;
+    resv += L;
+    Bp++;
+  }
   /* "if o_2 <= alpha, go to Phase TWO" (also: a single job, or one worker) */
-  if (k == 1 || I->B == 1 || I->len[S->pool[1]] <= a) return;
+  if (k == 1 || Bp == 1 || I->len[S->pool[1]] <= a) return;
   /* M = min{B, #{o_i > alpha}}; o_1 > o_2 > alpha so M >= 2 */
   int64_t m = 0;
   for (int32_t q = 0; q < k; ++q)
     if (I->len[S->pool[q]] > a) m++;
-  if (m > I->B) m = I->B;
+  if (m > Bp) m = Bp;
   const int64_t beta = (flags & FLAG_BETA_SQRT17) ? beta_sqrt17(a) : a;
   const int64_t o1 = I->len[S->pool[0]];
   /* cap_j = min{2 alpha, o_1 - o_j + beta} for the long workers j = 2..M;
-   * the spare workers j = M+1..B take packs of total at most alpha. */
-  for (int64_t w = 0; w < I->B; ++w) {
+   * the spare workers j = M+1..Bp take packs of total at most alpha. */
+  for (int64_t w = 0; w < Bp; ++w) {
     S->load[w] = 0;
     if (w >= 1 && w < m) {
       int64_t c1 = 2 * a, c2 = o1 - I->len[S->pool[w]] + beta;
@@ -310,7 +321,7 @@ static void phase_one(or_sim* S, const int32_t* ord_long, int64_t t, uint32_t fl
     int32_t j = S->pool[q];
     int64_t L = I->len[j];
     int64_t placed = -1;
-    for (int64_t w = m; w < I->B; ++w)
+    for (int64_t w = m; w < Bp; ++w)
       if (S->load[w] + L <= a) {
         placed = w;
         break;
@@ -332,7 +343,7 @@ static void phase_one(or_sim* S, const int32_t* ord_long, int64_t t, uint32_t fl
   /* Worker 1 idles for min{max{max_j P_j - alpha, 0}, alpha} (reading: the
    * largest pack sum; exact for B = 2, where it is Algorithm 2's delay). */
   int64_t pmax = 0;
-  for (int64_t w = 1; w < I->B; ++w)
+  for (int64_t w = 1; w < Bp; ++w)
     if (S->load[w] > pmax) pmax = S->load[w];
   int64_t idle = pmax - a;
   if (idle < 0) idle = 0;

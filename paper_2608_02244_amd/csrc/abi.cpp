@@ -1,0 +1,233 @@
+// C ABI of libfsched: argument checks, launch configuration, host staging.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "fsched.h"
+#include "sim_common.hpp"
+
+namespace {
+
+thread_local int g_last_hip = 0;
+
+int hip_fail(hipError_t e) {
+  g_last_hip = (int)e;
+  return e == hipErrorOutOfMemory ? FSCHED_ENOMEM : FSCHED_EDEVICE;
+}
+
+// floor((sqrt(17) - 1) alpha / 4): the largest k >= 0 with (4k + alpha)^2 <= 17 alpha^2.
+int32_t beta_sqrt17(int32_t alpha) {
+  long double approx = (sqrtl(17.0L) - 1.0L) * (long double)alpha / 4.0L;
+  int64_t k = (int64_t)approx;
+  if (k < 0) k = 0;
+  auto ok = [&](int64_t x) {
+    __int128 v = (__int128)(4 * x + alpha);
+    return v * v <= (__int128)17 * alpha * alpha;
+  };
+  while (ok(k + 1)) ++k;
+  while (k > 0 && !ok(k)) --k;
+  return (int32_t)k;
+}
+
+int check_params(const fsched_params* p, bool need_policy) {
+  if (!p) return FSCHED_EINVAL;
+  if (p->B < 0 || p->alpha < 0 || p->M_kv < 0 || p->cost_c < 0 || p->cost_tau < 0)
+    return FSCHED_EINVAL;
+  if (need_policy && (p->policy < FSCHED_FCFS || p->policy > FSCHED_SJF)) return FSCHED_EINVAL;
+  const uint32_t known = FSCHED_F_DEVICE_PTRS | FSCHED_F_SYNC | FSCHED_F_BETA_SQRT17;
+  if (p->flags & ~known) return FSCHED_EINVAL;
+  return FSCHED_OK;
+}
+
+int next_pow2(int x) {
+  int p = 64;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+// Map the per-instance markers of a finished host-mode call to a return code.
+int markers_to_code(const fsched_metrics* out, int64_t n_inst) {
+  int rc = FSCHED_OK;
+  for (int64_t i = 0; i < n_inst; ++i) {
+    int64_t T = out[i].T;
+    if (T >= 0) continue;
+    if (T == FSCHED_T_INVALID) return FSCHED_EINVAL;
+    if (T == FSCHED_T_RANGE) rc = FSCHED_ERANGE;
+    else if (T == FSCHED_T_TOOLARGE && rc == FSCHED_OK) rc = FSCHED_ETOOLARGE;
+    else if (rc == FSCHED_OK) rc = FSCHED_EINTERNAL;
+  }
+  return rc;
+}
+
+// Device copies of the host arrays of one call (host mode).
+struct Staging {
+  void* ptr[8] = {nullptr};
+  int n = 0;
+  hipError_t err = hipSuccess;
+  void* alloc(size_t bytes) {
+    void* d = nullptr;
+    if (err == hipSuccess) err = hipMalloc(&d, bytes ? bytes : 1);
+    if (err != hipSuccess) return nullptr;
+    ptr[n++] = d;
+    return d;
+  }
+  void* upload(const void* h, size_t bytes) {
+    void* d = alloc(bytes);
+    if (d && bytes) err = hipMemcpy(d, h, bytes, hipMemcpyHostToDevice);
+    return err == hipSuccess ? d : nullptr;
+  }
+  ~Staging() {
+    for (int i = 0; i < n; ++i) (void)hipFree(ptr[i]);
+  }
+};
+
+int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int32_t* arrival,
+                    const int32_t* prompt, const int32_t* output, fsched_metrics* out,
+                    int32_t* start, int32_t* finish, hipStream_t s) {
+  const int Beff = (p->B == 0 || p->B > n) ? n : p->B;
+  if (n > fs::MAX_JOBS || Beff > fs::MAX_WORKERS) return FSCHED_ETOOLARGE;
+  int K = 1;
+  while (K * 64 < Beff) K <<= 1;
+  const int NW = n <= 2048 ? 1 : 2;
+  const int NP = next_pow2(n);
+  const bool isjl = p->policy == FSCHED_ISJL;
+  const int q_words = isjl ? NP / 2 : 0;
+  const int stage_words = isjl ? (Beff + 1) / 2 : 0;
+
+  fs::SimArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.n_inst = n_inst;
+  a.n = n;
+  a.Beff = Beff;
+  a.alpha = p->alpha;
+  a.beta = (p->flags & FSCHED_F_BETA_SQRT17) ? beta_sqrt17(p->alpha) : p->alpha;
+  a.M = p->M_kv;
+  a.c = p->cost_c;
+  a.tau = p->cost_tau;
+  a.NP = NP;
+  a.arrival = arrival;
+  a.prompt = prompt;
+  a.output = output;
+  a.out = out;
+  a.start = start;
+  a.finish = finish;
+
+  for (int general = 0; general < 2; ++general) {
+    fs::SimArgs b = a;
+    b.off_arr = NP;
+    b.off_q = NP + (general ? NP : 0);
+    b.off_stage = b.off_q + q_words;
+    b.wave_words = b.off_stage + stage_words;
+    b.wave_words = (b.wave_words + 3) & ~3;
+    size_t per_wave = (size_t)b.wave_words * 4;
+    int wpb = 4;
+    while (wpb > 1 && per_wave * wpb > 64 * 1024) wpb >>= 1;
+    size_t lds = per_wave * wpb;
+    hipError_t e;
+    switch (p->policy) {
+      case FSCHED_FCFS: e = fs::launch_sim_fcfs(b, K, NW, general, wpb, lds, s); break;
+      case FSCHED_LJF: e = fs::launch_sim_ljf(b, K, NW, general, wpb, lds, s); break;
+      case FSCHED_ISJL: e = fs::launch_sim_isjl(b, K, NW, general, wpb, lds, s); break;
+      default: e = fs::launch_sim_sjf(b, K, NW, general, wpb, lds, s); break;
+    }
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  return FSCHED_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* fsched_strerror(int code) {
+  switch (code) {
+    case FSCHED_OK: return "ok";
+    case FSCHED_EINVAL: return "invalid argument or job table";
+    case FSCHED_ERANGE: return "an int64 accumulator could overflow";
+    case FSCHED_ENOMEM: return "out of memory";
+    case FSCHED_EDEVICE: return "HIP runtime error";
+    case FSCHED_ETOOLARGE: return "instance beyond a kernel limit";
+    case FSCHED_ENOTIMPL: return "not implemented";
+    case FSCHED_EINTERNAL: return "internal error: no next event";
+    default: return "unknown error code";
+  }
+}
+
+int fsched_abi_version(void) { return FSCHED_ABI_VERSION; }
+
+int fsched_last_hip_error(void) { return g_last_hip; }
+
+int fsched_simulate(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
+                    const int32_t* arrival, const int32_t* prompt, const int32_t* output,
+                    fsched_metrics* out, int32_t* start, int32_t* finish, void* stream) {
+  int rc = check_params(p, true);
+  if (rc) return rc;
+  if (n_inst < 0 || n_jobs < 1) return FSCHED_EINVAL;
+  if (n_inst == 0) return FSCHED_OK;
+  if (!arrival || !prompt || !output || !out) return FSCHED_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  if (p->flags & FSCHED_F_DEVICE_PTRS) {
+    rc = launch_simulate(p, n_inst, n_jobs, arrival, prompt, output, out, start, finish, s);
+    if (rc) return rc;
+    if (p->flags & FSCHED_F_SYNC) {
+      hipError_t e = hipStreamSynchronize(s);
+      if (e != hipSuccess) return hip_fail(e);
+    }
+    return FSCHED_OK;
+  }
+  const size_t cells = (size_t)n_inst * (size_t)n_jobs;
+  const size_t tb = cells * sizeof(int32_t);
+  Staging st;
+  const int32_t* da = (const int32_t*)st.upload(arrival, tb);
+  const int32_t* dp = (const int32_t*)st.upload(prompt, tb);
+  const int32_t* dq = (const int32_t*)st.upload(output, tb);
+  fsched_metrics* dout = (fsched_metrics*)st.alloc((size_t)n_inst * sizeof(fsched_metrics));
+  int32_t* dst = start ? (int32_t*)st.alloc(tb) : nullptr;
+  int32_t* dfi = finish ? (int32_t*)st.alloc(tb) : nullptr;
+  if (st.err != hipSuccess) return hip_fail(st.err);
+  rc = launch_simulate(p, n_inst, n_jobs, da, dp, dq, dout, dst, dfi, s);
+  if (rc) return rc;
+  hipError_t e = hipStreamSynchronize(s);
+  if (e == hipSuccess)
+    e = hipMemcpy(out, dout, (size_t)n_inst * sizeof(fsched_metrics), hipMemcpyDeviceToHost);
+  if (e == hipSuccess && start) e = hipMemcpy(start, dst, tb, hipMemcpyDeviceToHost);
+  if (e == hipSuccess && finish) e = hipMemcpy(finish, dfi, tb, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e);
+  return markers_to_code(out, n_inst);
+}
+
+int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
+                          const int32_t* arrival, const int32_t* prompt, const int32_t* output,
+                          const int32_t* start, fsched_metrics* out, uint32_t* violation,
+                          void* stream) {
+  (void)p;
+  (void)n_inst;
+  (void)n_jobs;
+  (void)arrival;
+  (void)prompt;
+  (void)output;
+  (void)start;
+  (void)out;
+  (void)violation;
+  (void)stream;
+  return FSCHED_ENOTIMPL;
+}
+
+int fsched_bruteforce_opt(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
+                          const int32_t* arrival, const int32_t* prompt, const int32_t* output,
+                          int64_t* T_opt, int32_t* start_opt, void* stream) {
+  (void)p;
+  (void)n_inst;
+  (void)n_jobs;
+  (void)arrival;
+  (void)prompt;
+  (void)output;
+  (void)T_opt;
+  (void)start_opt;
+  (void)stream;
+  return FSCHED_ENOTIMPL;
+}
+
+}  // extern "C"

@@ -1,0 +1,10 @@
+// Kernel instantiations for the ISJL policy (one translation unit per policy so
+// that they compile in parallel).
+#include "sim_kernel.hpp"
+
+namespace fs {
+hipError_t launch_sim_isjl(const SimArgs& a, int K, int NW, bool general, int waves_per_block,
+                         size_t lds_bytes, hipStream_t s) {
+  return launch_sim<POL_ISJL>(a, K, NW, general, waves_per_block, lds_bytes, s);
+}
+}  // namespace fs

@@ -1,0 +1,880 @@
+// Batched evaluation of the token-step scheduling model: one wavefront per
+// instance.
+//
+// Model (Section 2): job i needs len_i = prompt_i + output_i steps; a job
+// started at step s is active on s .. s+len-1; at most B jobs per step; the
+// fairness constraint eq. (1) bounds the progress spread of co-running jobs by
+// alpha; a KV budget M_kv bounds the summed reservations of co-running jobs.
+// Policies: FCFS / SJF (Section 2.1 baselines), LJF (Algorithm 1) and ISJL
+// (Algorithms 2 and 3 on the released queue, Section 3.5).  Costs: Section 5.
+//
+// The kernel is event driven.  Between two events (a completion, a release, a
+// delayed plan start, or the step at which A_max(t) crosses alpha while Phase
+// TWO waits on the KV budget) the active set is fixed and every active job
+// advances one token per step, so the per-step terms of Section 5 are
+// arithmetic series summed in closed form:
+//   max r over [t, t+D): m_t = t - min_s + 1, sum = D m_t + D(D-1)/2
+//   E per step  = sum_S (m_t - r_i) = sum_s - |S| min_s       (constant)
+//   extent      = max_s - min_s                               (constant)
+//   sum_S r     = |S| (t+1) - sum_s                            (largest at t+D-1)
+// Decisions are taken only at events; the step-by-step definition gives the
+// same decisions at the steps in between because nothing they depend on
+// changes there.
+//
+// Per-wave state:
+//   LDS   W[r]     jobs in the policy's priority order, packed (len << 12 | id)
+//         ARR[r]   arrival of rank r (general variant only)
+//         QN[r]    next job in the same ISJL plan queue (uint16, ISJL)
+//         STG[j]   gather buffer for Phase ONE (uint16, ISJL)
+//   VGPR  K worker slots per lane: worker w lives in slot w/64 of lane w%64
+//         (start, end, ISJL plan-queue head|tail); a bitmap of queued jobs over
+//         ranks (bit r%32 of word r/2048 in lane (r/32)%64).
+//   SGPR  time, counters, cost accumulators.
+#pragma once
+#include "sim_common.hpp"
+#include "wave.hpp"
+
+namespace fs {
+
+constexpr int POL_FCFS = FSCHED_FCFS, POL_LJF = FSCHED_LJF, POL_ISJL = FSCHED_ISJL,
+              POL_SJF = FSCHED_SJF;
+constexpr int IDLE = 0x7FFFFFFF;
+constexpr uint32_t QNONE = 0xFFFFu;
+constexpr uint32_t LMASK = 0xFFFFFu;
+
+__device__ __forceinline__ int plen(uint32_t w) { return (int)(w >> 12); }
+__device__ __forceinline__ int pid(uint32_t w) { return (int)(w & 0xFFFu); }
+
+// Bitonic sort of NP (power of two) keys in LDS, ascending, by one wave.
+__device__ inline void wave_bitonic_sort(uint32_t* W, int NP, int lane) {
+  for (int k = 2; k <= NP; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = lane; i < (NP >> 1); i += WAVE) {
+        int lo = ((i & ~(j - 1)) << 1) | (i & (j - 1));
+        int hi = lo + j;
+        bool up = (lo & k) == 0;
+        uint32_t x = W[lo], y = W[hi];
+        if ((x > y) == up) {
+          W[lo] = y;
+          W[hi] = x;
+        }
+      }
+      wave_lds_sync();
+    }
+  }
+}
+
+__device__ inline void write_marker(fsched_metrics* out, int64_t inst, int64_t code, int lane) {
+  if (lane == 0) {
+    fsched_metrics m;
+    m.T = code;
+    m.O = m.Q = m.E = m.C = m.W = 0;
+    m.sum_completion = m.sum_latency = m.sum_extent = m.busy_steps = 0;
+    m.peak_kv = m.unfair_steps = 0;
+    m.max_extent = m.max_active = 0;
+    out[inst] = m;
+  }
+}
+
+template <int NW>
+struct PoolBits {
+  uint32_t w[NW];
+
+  __device__ __forceinline__ void clear_all() {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) w[i] = 0u;
+  }
+  // first set rank, -1 if none
+  __device__ __forceinline__ int first() const {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      uint64_t m = ballot(w[i] != 0u);
+      if (m) {
+        int L = __builtin_ctzll(m);
+        uint32_t x = (uint32_t)readlane((int)w[i], L);
+        return ((i * WAVE + L) << 5) + __builtin_ctz(x);
+      }
+    }
+    return -1;
+  }
+  // first set rank >= r0, -1 if none
+  __device__ __forceinline__ int first_from(int r0, int lane) const {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      int base = (i * WAVE + lane) << 5;
+      uint32_t x = w[i];
+      if (base + 32 <= r0) x = 0u;
+      else if (base < r0) x &= ~((1u << (r0 - base)) - 1u);
+      uint64_t m = ballot(x != 0u);
+      if (m) {
+        int L = __builtin_ctzll(m);
+        uint32_t y = (uint32_t)readlane((int)x, L);
+        return ((i * WAVE + L) << 5) + __builtin_ctz(y);
+      }
+    }
+    return -1;
+  }
+  __device__ __forceinline__ void set(int r, int lane) {
+    int L = (r >> 5) & (WAVE - 1), wi = r >> 11;
+    uint32_t b = 1u << (r & 31);
+#pragma unroll
+    for (int i = 0; i < NW; ++i)
+      if (i == wi && lane == L) w[i] |= b;
+  }
+  __device__ __forceinline__ void reset(int r, int lane) {
+    int L = (r >> 5) & (WAVE - 1), wi = r >> 11;
+    uint32_t b = 1u << (r & 31);
+#pragma unroll
+    for (int i = 0; i < NW; ++i)
+      if (i == wi && lane == L) w[i] &= ~b;
+  }
+  // clear every rank <= r
+  __device__ __forceinline__ void clear_upto(int r, int lane) {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      int base = (i * WAVE + lane) << 5;
+      if (base + 31 <= r) w[i] = 0u;
+      else if (base <= r) w[i] &= ~((2u << (r - base)) - 1u);
+    }
+  }
+  __device__ __forceinline__ int count() const {
+    int c = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) c += __builtin_popcount(w[i]);
+    return wave_sum(c);
+  }
+};
+
+// Wave-uniform scalars of one instance.
+struct SimState {
+  int t, ndone, nact, min_s, max_s, min_end;
+  int64_t res, sum_s, sum_comp;
+};
+
+template <int POL, int K, int NW, bool GEN>
+__global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
+  extern __shared__ uint32_t lds_raw[];
+  const int wib = threadIdx.x >> 6;
+  const int64_t inst = (int64_t)blockIdx.x * (blockDim.x >> 6) + wib;
+  if (inst >= a.n_inst) return;
+  const int lane = lane_id();
+  const int n = a.n;
+  uint32_t* W = lds_raw + (size_t)wib * (size_t)a.wave_words;
+  int32_t* ARR = (int32_t*)(W + a.off_arr);
+  uint16_t* QN = (uint16_t*)(W + a.off_q);
+  uint16_t* STG = (uint16_t*)(W + a.off_stage);
+  const int64_t row = inst * (int64_t)n;
+  const int32_t* A = a.arrival + row;
+  const int32_t* P = a.prompt + row;
+  const int32_t* O = a.output + row;
+
+  if (GEN) {
+    if (a.out[inst].T != T_DEFERRED) return;  // the sorted-arrival kernel handled it
+  }
+
+  // ---- load, validate, instance constants --------------------------------
+  int bad = 0, big = 0, unsorted = 0, maxlen = 0, maxarr = 0;
+  int64_t osum = 0, qsum = 0, rsum = 0;
+  for (int i = lane; i < n; i += WAVE) {
+    int ar = A[i], p = P[i], o = O[i];
+    bad |= (ar < 0) | (p < 0) | (o < 1);
+    int64_t len = (int64_t)p + (int64_t)o;
+    big |= (len >= LEN_LIMIT);
+    if (i > 0) unsorted |= (A[i - 1] > ar);
+    if (len < LEN_LIMIT && len > maxlen) maxlen = (int)len;
+    if (ar > maxarr) maxarr = ar;
+    osum += len;
+    qsum += len * (len + 1) / 2;
+    rsum += ar;
+  }
+  bad = ballot(bad != 0) != 0;
+  big = ballot(big != 0) != 0;
+  unsorted = ballot(unsorted != 0) != 0;
+  if (bad) {
+    write_marker(a.out, inst, FSCHED_T_INVALID, lane);
+    return;
+  }
+  if (big) {
+    write_marker(a.out, inst, FSCHED_T_TOOLARGE, lane);
+    return;
+  }
+  if (!GEN && unsorted) {
+    write_marker(a.out, inst, T_DEFERRED, lane);
+    return;
+  }
+  maxlen = wave_max(maxlen);
+  maxarr = wave_max(maxarr);
+  osum = wave_sum64(osum);
+  qsum = wave_sum64(qsum);
+  rsum = wave_sum64(rsum);
+  if (GEN && maxarr >= ARR_LIMIT) {
+    write_marker(a.out, inst, FSCHED_T_TOOLARGE, lane);
+    return;
+  }
+  {
+    // Largest makespan any policy here can reach: all work serialised after the
+    // last release, plus one delayed plan start (<= alpha) per job.
+    double amin = a.alpha < maxlen ? (double)a.alpha : (double)maxlen;
+    double tb = (double)maxarr + (double)osum + (double)n * amin + 1.0;
+    if (tb >= 2147483000.0) {
+      write_marker(a.out, inst, FSCHED_T_TOOLARGE, lane);
+      return;
+    }
+    double cb = (double)a.c * tb + (double)a.tau * (double)osum * (double)maxlen;
+    double wb = (double)a.c * tb + (double)a.tau * tb * (double)maxlen;
+    if (cb > 4.0e18 || wb > 4.0e18) {
+      write_marker(a.out, inst, FSCHED_T_RANGE, lane);
+      return;
+    }
+  }
+
+  // ---- priority order -----------------------------------------------------
+  // LJF / ISJL: (-len, index); SJF: (len, index); FCFS: (arrival, index).
+  const int NP = a.NP;
+  if (POL == POL_FCFS && !GEN) {
+    for (int r = lane; r < n; r += WAVE) W[r] = ((uint32_t)(P[r] + O[r]) << 12) | (uint32_t)r;
+  } else {
+    for (int r = lane; r < NP; r += WAVE) {
+      uint32_t key = 0xFFFFFFFFu;
+      if (r < n) {
+        uint32_t len = (uint32_t)(P[r] + O[r]);
+        if (POL == POL_LJF || POL == POL_ISJL) key = ((LMASK - len) << 12) | (uint32_t)r;
+        else if (POL == POL_SJF) key = (len << 12) | (uint32_t)r;
+        else key = ((uint32_t)A[r] << 12) | (uint32_t)r;
+      }
+      W[r] = key;
+    }
+    wave_lds_sync();
+    wave_bitonic_sort(W, NP, lane);
+    for (int r = lane; r < n; r += WAVE) {
+      uint32_t key = W[r];
+      int id = (int)(key & 0xFFFu);
+      uint32_t len;
+      if (POL == POL_LJF || POL == POL_ISJL) len = LMASK - (key >> 12);
+      else if (POL == POL_SJF) len = key >> 12;
+      else len = (uint32_t)(P[id] + O[id]);
+      W[r] = (len << 12) | (uint32_t)id;
+      if (GEN) ARR[r] = A[id];
+    }
+  }
+  wave_lds_sync();
+
+  // ---- state ---------------------------------------------------------------
+  const int Beff = a.Beff;
+  const int alpha = a.alpha;
+  const int64_t M = a.M;
+  int ws_start[K], ws_end[K];
+  uint32_t ws_q[K];
+  bool valid[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    ws_start[k] = IDLE;
+    ws_end[k] = IDLE;
+    ws_q[k] = QNONE | (QNONE << 16);
+    valid[k] = (k * WAVE + lane) < Beff;
+  }
+  PoolBits<NW> pool;
+  pool.clear_all();
+  PoolBits<NW> unrel;  // general variant, non-FCFS: ranks not yet released
+  unrel.clear_all();
+  if (GEN && POL != POL_FCFS) {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      int base = (i * WAVE + lane) << 5;
+      uint32_t m = 0u;
+      if (base + 32 <= n) m = 0xFFFFFFFFu;
+      else if (base < n) m = (1u << (n - base)) - 1u;
+      unrel.w[i] = m;
+    }
+  }
+  int relk = 0;           // release cursor
+  int chunk = -1;         // release chunk loaded in rel_t / rel_r
+  int rel_t = IDLE, rel_r = 0;
+  int next_rel = 0;       // general variant, non-FCFS
+  int head = 0;           // FCFS: first waiting rank
+  // ISJL
+  int mode = 0;           // 0 FILL, 1 DRAIN
+  int planned = 0;        // planned jobs not yet started
+  int t_w1 = 0;           // earliest start of worker 0's planned job
+
+  SimState S;
+  S.t = 0;
+  S.ndone = 0;
+  S.nact = 0;
+  S.min_s = IDLE;
+  S.max_s = -1;
+  S.min_end = IDLE;
+  S.res = 0;
+  S.sum_s = 0;
+  S.sum_comp = 0;
+  int64_t acc_E = 0, acc_C = 0, acc_W = 0, acc_ext = 0, acc_busy = 0, acc_peak = 0, acc_unfair = 0;
+  int acc_maxext = 0, acc_maxact = 0;
+  int32_t* st_out = a.start ? a.start + row : nullptr;
+  int32_t* fi_out = a.finish ? a.finish + row : nullptr;
+  const int iter_max = 8 * n + 64;
+  int iter = 0;
+  bool failed = false;
+
+  // Load release chunk `c` (64 consecutive jobs in arrival order).
+  auto load_chunk = [&](int c) {
+    int j = c * WAVE + lane;
+    rel_t = IDLE;
+    rel_r = 0;
+    if (POL == POL_FCFS) {
+      if (j < n) rel_t = GEN ? ARR[j] : A[j];
+      rel_r = j;
+    } else if (j < n) {
+      // rank of job j: position of its priority key in W (binary search)
+      rel_t = A[j];
+      uint32_t len = (uint32_t)(P[j] + O[j]);
+      uint32_t key;
+      if (POL == POL_SJF) key = (len << 12) | (uint32_t)j;
+      else key = ((LMASK - len) << 12) | (uint32_t)j;
+      int lo = 0, hi = n;  // first rank whose key >= key
+      while (lo < hi) {
+        int mid = (lo + hi) >> 1;
+        uint32_t wv = W[mid];
+        uint32_t kv = (POL == POL_SJF) ? wv : (((LMASK - (wv >> 12)) << 12) | (wv & 0xFFFu));
+        if (kv < key) lo = mid + 1;
+        else hi = mid;
+      }
+      rel_r = lo;
+    }
+    chunk = c;
+  };
+
+  // Schedule output of one admitted job.
+  auto emit = [&](int id, int t, int len) {
+    if (st_out) st_out[id] = t;
+    if (fi_out) fi_out[id] = t + len;
+  };
+
+  while (true) {
+    const int t = S.t;
+    // (1) retire the jobs whose last token was processed at t-1
+    if (S.min_end == t) {
+      int cnt = 0, lsum = 0, me = IDLE, mn = IDLE, mx = -1;
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        if (ws_end[k] == t) {
+          cnt++;
+          lsum += ws_end[k] - ws_start[k];
+          ws_end[k] = IDLE;
+          ws_start[k] = IDLE;
+        }
+        me = min(me, ws_end[k]);
+        mn = min(mn, ws_start[k]);
+        if (ws_start[k] != IDLE) mx = max(mx, ws_start[k]);
+      }
+      int nret = wave_sum(cnt);
+      int lret = wave_sum(lsum);
+      S.min_end = wave_min(me);
+      S.min_s = wave_min(mn);
+      S.max_s = wave_max(mx);
+      S.ndone += nret;
+      S.nact -= nret;
+      S.res -= lret;
+      S.sum_s -= (int64_t)nret * t - (int64_t)lret;
+    }
+    if (S.ndone == n) break;
+
+    // (2) releases
+    if (POL == POL_FCFS) {
+      while (relk < n) {
+        if ((relk >> 6) != chunk) load_chunk(relk >> 6);
+        int rt = readlane(rel_t, relk & 63);
+        if (rt > t) break;
+        relk++;
+      }
+    } else if (!GEN) {
+      while (relk < n) {
+        if ((relk >> 6) != chunk) load_chunk(relk >> 6);
+        int rt = readlane(rel_t, relk & 63);
+        if (rt > t) break;
+        pool.set(readlane(rel_r, relk & 63), lane);
+        relk++;
+      }
+    } else if (next_rel <= t) {
+      int nr = IDLE;
+#pragma unroll
+      for (int i = 0; i < NW; ++i) {
+        uint32_t u = unrel.w[i], got = 0u;
+        int base = (i * WAVE + lane) << 5;
+        while (u) {
+          int b = __builtin_ctz(u);
+          u &= u - 1u;
+          int ar = ARR[base + b];
+          if (ar <= t) got |= 1u << b;
+          else nr = min(nr, ar);
+        }
+        unrel.w[i] &= ~got;
+        pool.w[i] |= got;
+      }
+      next_rel = wave_min(nr);
+    }
+
+    // (3) A_max(t): largest progress among the jobs still active
+    const int amax = S.nact > 0 ? t - S.min_s : 0;
+    const int nact0 = S.nact;
+    int adm = 0, adm_minlen = IDLE;
+    int64_t adm_len = 0;
+    bool kv_block = false;
+
+    // (4) admissions
+    if (POL == POL_FCFS) {
+      int cnt = min(relk - head, Beff - S.nact);
+      int done = 0;
+      while (done < cnt) {
+        int c = min(WAVE, cnt - done);
+        int r = head + done + lane;
+        uint32_t wv = lane < c ? W[r] : 0u;
+        int len = plen(wv), id = pid(wv);
+        int pre = wave_scan_incl(len);
+        bool fit = (M == 0) || ((int64_t)(S.res + pre) <= M) ||
+                   (S.nact == 0 && done == 0 && lane == 0);
+        uint64_t fm = ballot(lane < c && !fit);
+        int take = fm ? __builtin_ctzll(fm) : c;
+        if (take > 0) {
+          int base = 0;
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            if (base < take) {
+              bool idle = valid[k] && ws_end[k] == IDLE;
+              uint64_t bm = ballot(idle);
+              int idx = base + mbcnt(bm);
+              int src = min(idx, WAVE - 1);
+              int l2 = __shfl(len, src), id2 = __shfl(id, src);
+              if (idle && idx < take) {
+                ws_start[k] = t;
+                ws_end[k] = t + l2;
+                emit(id2, t, l2);
+              }
+              base += __builtin_popcountll(bm);
+            }
+          }
+          int tl = readlane(pre, take - 1);
+          adm_minlen = min(adm_minlen, wave_min(lane < take ? len : IDLE));
+          adm += take;
+          adm_len += tl;
+          S.res += tl;
+          S.nact += take;
+        }
+        done += take;
+        if (take < c) break;
+      }
+      head += done;
+    } else if (POL == POL_LJF || POL == POL_SJF) {
+      if (POL == POL_SJF || S.nact == 0) {
+        while (S.nact < Beff) {
+          int r = pool.first();
+          if (r < 0) break;
+          uint32_t wv = W[r];
+          int len = plen(wv);
+          if (M != 0 && S.nact > 0 && S.res + len > M) break;
+          pool.reset(r, lane);
+          int slot = -1;
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            if (slot < 0) {
+              uint64_t bm = ballot(valid[k] && ws_end[k] == IDLE);
+              if (bm) slot = k * WAVE + __builtin_ctzll(bm);
+            }
+          }
+#pragma unroll
+          for (int k = 0; k < K; ++k)
+            if (k == (slot >> 6) && lane == (slot & 63)) {
+              ws_start[k] = t;
+              ws_end[k] = t + len;
+            }
+          if (lane == 0) emit(pid(wv), t, len);
+          adm++;
+          adm_len += len;
+          adm_minlen = min(adm_minlen, len);
+          S.res += len;
+          S.nact++;
+        }
+      }
+    } else {  // ISJL
+      // Epoch: empty machine, nothing planned, jobs queued -> Phase ONE.
+      if (S.nact == 0 && planned == 0) {
+        int kp = pool.count();
+        if (kp > 0) {
+          mode = 0;
+          int G = min(Beff, kp);
+          // gather the first G queued ranks (longest first) into STG
+          {
+            int gbase = 0;
+#pragma unroll
+            for (int i = 0; i < NW; ++i) {
+              int cnt = __builtin_popcount(pool.w[i]);
+              int incl = wave_scan_incl(cnt);
+              int pos = gbase + incl - cnt;
+              uint32_t x = pool.w[i];
+              int base = (i * WAVE + lane) << 5;
+              while (x && pos < G) {
+                int b = __builtin_ctz(x);
+                x &= x - 1u;
+                STG[pos] = (uint16_t)(base + b);
+                pos++;
+              }
+              gbase += readlane(incl, 63);
+            }
+            wave_lds_sync();
+          }
+          // Bp: largest prefix of the longest jobs that fits the KV budget
+          int Bp = G;
+          if (M != 0) {
+            int64_t run = 0;
+            for (int c0 = 0; c0 < G; c0 += WAVE) {
+              int j = c0 + lane;
+              int len = j < G ? plen(W[STG[j]]) : 0;
+              int pre = wave_scan_incl(len);
+              uint64_t fm = ballot(j < G && j >= 1 && run + pre > M);
+              if (fm) {
+                Bp = c0 + __builtin_ctzll(fm);
+                break;
+              }
+              run += readlane(pre, 63);
+            }
+            if (Bp < 1) Bp = 1;
+          }
+          int o2 = kp > 1 ? plen(W[STG[1]]) : 0;
+          if (kp > 1 && Bp > 1 && o2 > alpha) {
+            // M = min{Bp, #{len > alpha}} (a prefix of the sorted queue)
+            int m = 0;
+            for (int c0 = 0; c0 < Bp; c0 += WAVE) {
+              int j = c0 + lane;
+              bool lng = j < Bp && plen(W[STG[j]]) > alpha;
+              m += __builtin_popcountll(ballot(lng));
+            }
+            const int o1 = plen(W[STG[0]]);
+            const int beta = a.beta;
+            int cap[K], load[K];
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              int w = k * WAVE + lane;
+              load[k] = 0;
+              if (w >= 1 && w < m) {
+                int lj = plen(W[STG[w]]);
+                cap[k] = min(2 * alpha, o1 - lj + beta);
+              } else if (w >= m && w < Bp) {
+                cap[k] = alpha;
+              } else {
+                cap[k] = -1;
+              }
+            }
+            // the m long jobs are the first m queued ranks
+            const int rlast = STG[m - 1];
+            pool.clear_upto(rlast, lane);
+            planned += m;
+            // Pack scan (Algorithm 3): remaining queued jobs in decreasing length;
+            // each goes to the first spare worker with room, else to the long
+            // worker of largest index with room; a job that fits nowhere stays.
+            int cur = rlast;
+            while (true) {
+              int rm = -1;
+#pragma unroll
+              for (int k = 0; k < K; ++k) rm = max(rm, cap[k] - load[k]);
+              int remmax = wave_max(rm);
+              if (remmax <= 0) break;
+              int r = pool.first_from(cur + 1, lane);
+              if (r < 0) break;
+              int len = plen(W[r]);
+              if (len > remmax) {
+                // first rank >= r with len <= remmax (lengths are non-increasing)
+                int span = n - r;
+                int s = (span + WAVE - 1) / WAVE;
+                int p = r + lane * s;
+                bool ok = p < n && plen(W[p]) <= remmax;
+                uint64_t fm = ballot(ok);
+                int lo, hi;
+                if (fm) {
+                  int L1 = __builtin_ctzll(fm);
+                  hi = r + L1 * s;
+                  lo = L1 > 0 ? r + (L1 - 1) * s + 1 : r;
+                } else {
+                  lo = r + 63 * s + 1;
+                  hi = n;
+                }
+                int q = lo + lane;
+                bool ok2 = q < hi && plen(W[q]) <= remmax;
+                uint64_t fm2 = ballot(ok2);
+                int b = fm2 ? lo + __builtin_ctzll(fm2) : hi;
+                if (b >= n) break;
+                r = pool.first_from(b, lane);
+                if (r < 0) break;
+                len = plen(W[r]);
+              }
+              int wsel = -1;
+#pragma unroll
+              for (int k = 0; k < K; ++k) {
+                int w = k * WAVE + lane;
+                uint64_t ms = ballot(w >= m && w < Bp && cap[k] - load[k] >= len);
+                if (wsel < 0 && ms) wsel = k * WAVE + __builtin_ctzll(ms);
+              }
+              if (wsel < 0) {
+#pragma unroll
+                for (int k = K - 1; k >= 0; --k) {
+                  int w = k * WAVE + lane;
+                  uint64_t ml = ballot(w >= 1 && w < m && cap[k] - load[k] >= len);
+                  if (wsel < 0 && ml) wsel = k * WAVE + 63 - __builtin_clzll(ml);
+                }
+              }
+              if (wsel < 0) break;  // unreachable: len <= remmax
+              // append r to worker wsel's queue
+              int qt = (int)QNONE;
+#pragma unroll
+              for (int k = 0; k < K; ++k)
+                if (k == (wsel >> 6)) qt = readlane((int)(ws_q[k] >> 16), wsel & 63);
+              if (lane == 0) {
+                if (qt != (int)QNONE) QN[qt] = (uint16_t)r;
+                QN[r] = (uint16_t)QNONE;
+              }
+#pragma unroll
+              for (int k = 0; k < K; ++k)
+                if (k == (wsel >> 6) && lane == (wsel & 63)) {
+                  load[k] += len;
+                  uint32_t h = ws_q[k] & 0xFFFFu;
+                  if (h == QNONE) h = (uint32_t)r;
+                  ws_q[k] = h | ((uint32_t)r << 16);
+                }
+              pool.reset(r, lane);
+              planned++;
+              cur = r;
+            }
+            wave_lds_sync();
+            // worker j in 2..M: its pack, then o_j; worker 1: o_1
+            int pmax = 0;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              int w = k * WAVE + lane;
+              if (w >= 1 && w < Bp) pmax = max(pmax, load[k]);
+              if (w >= 1 && w < m) {
+                uint32_t r = STG[w];
+                uint32_t h = ws_q[k] & 0xFFFFu, tl = ws_q[k] >> 16;
+                if (tl != QNONE) QN[tl] = (uint16_t)r;
+                else h = r;
+                QN[r] = (uint16_t)QNONE;
+                ws_q[k] = h | (r << 16);
+              }
+              if (w == 0) {
+                uint32_t r = STG[0];
+                QN[r] = (uint16_t)QNONE;
+                ws_q[k] = r | (r << 16);
+              }
+            }
+            wave_lds_sync();
+            pmax = wave_max(pmax);
+            int idle1 = pmax - alpha;
+            if (idle1 < 0) idle1 = 0;
+            if (idle1 > alpha) idle1 = alpha;
+            t_w1 = t + idle1;
+          }
+        }
+      }
+      // Plan starts (workers in index order), each guarded by
+      // A_max(t) <= alpha and the KV budget.
+      if (planned > 0 && amax <= alpha) {
+        bool cand[K];
+        int clen[K];
+        int csum = 0, ccnt = 0;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          int w = k * WAVE + lane;
+          uint32_t h = ws_q[k] & 0xFFFFu;
+          cand[k] = valid[k] && ws_end[k] == IDLE && h != QNONE && !(w == 0 && t < t_w1);
+          clen[k] = cand[k] ? plen(W[h]) : 0;
+          csum += clen[k];
+          ccnt += cand[k] ? 1 : 0;
+        }
+        int tot = wave_sum(csum);
+        int ncand = wave_sum(ccnt);
+        if (ncand > 0) {
+          bool all = (M == 0) || (S.res + tot <= M) || (S.nact == 0 && ncand == 1);
+          if (!all) {
+            // Sequential KV check in worker order; a blocked worker waits and
+            // later workers are still tried.
+            int nk = 0;
+            int64_t rres = S.res;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              uint64_t mk = ballot(cand[k]);
+              uint64_t keep = 0;
+              while (mk) {
+                int L = __builtin_ctzll(mk);
+                mk &= mk - 1;
+                int len = readlane(clen[k], L);
+                if (S.nact + nk == 0 || rres + len <= M) {
+                  keep |= 1ull << L;
+                  rres += len;
+                  nk++;
+                }
+              }
+              cand[k] = cand[k] && ((keep >> lane) & 1ull);
+            }
+            tot = (int)(rres - S.res);
+            ncand = nk;
+          }
+          int mlen = IDLE;
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            if (cand[k]) {
+              uint32_t h = ws_q[k] & 0xFFFFu;
+              uint32_t wv = W[h];
+              int len = plen(wv);
+              ws_start[k] = t;
+              ws_end[k] = t + len;
+              mlen = min(mlen, len);
+              emit(pid(wv), t, len);
+              uint32_t nx = QN[h];
+              ws_q[k] = (nx == QNONE) ? (QNONE | (QNONE << 16)) : (nx | (ws_q[k] & 0xFFFF0000u));
+            }
+          }
+          adm_minlen = min(adm_minlen, wave_min(mlen));
+          adm += ncand;
+          adm_len += tot;
+          S.res += tot;
+          S.nact += ncand;
+          planned -= ncand;
+        }
+      }
+      // Phase TWO (FILL): idle workers with nothing planned take the longest
+      // queued unplanned job while A_max(t) <= alpha; otherwise DRAIN.
+      if (mode == 0) {
+        while (true) {
+          int wsel = -1;
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            uint64_t bm = ballot(valid[k] && ws_end[k] == IDLE && (ws_q[k] & 0xFFFFu) == QNONE);
+            if (wsel < 0 && bm) wsel = k * WAVE + __builtin_ctzll(bm);
+          }
+          if (wsel < 0) break;
+          int r = pool.first();
+          if (r < 0) break;
+          if (amax > alpha) {
+            mode = 1;
+            break;
+          }
+          uint32_t wv = W[r];
+          int len = plen(wv);
+          if (M != 0 && S.nact > 0 && S.res + len > M) {
+            kv_block = true;
+            break;
+          }
+          pool.reset(r, lane);
+#pragma unroll
+          for (int k = 0; k < K; ++k)
+            if (k == (wsel >> 6) && lane == (wsel & 63)) {
+              ws_start[k] = t;
+              ws_end[k] = t + len;
+            }
+          if (lane == 0) emit(pid(wv), t, len);
+          adm++;
+          adm_len += len;
+          adm_minlen = min(adm_minlen, len);
+          S.res += len;
+          S.nact++;
+        }
+      }
+    }
+    if (adm > 0) {
+      S.sum_s += (int64_t)adm * t;
+      S.sum_comp += (int64_t)adm * t + adm_len;
+      S.min_end = min(S.min_end, t + adm_minlen);
+      if (nact0 == 0) S.min_s = t;
+      S.max_s = t;
+    }
+
+    // (5) next event
+    int tn = S.min_end;
+    if (POL == POL_FCFS || !GEN) {
+      if (relk < n) {
+        if ((relk >> 6) != chunk) load_chunk(relk >> 6);
+        tn = min(tn, readlane(rel_t, relk & 63));
+      }
+    } else {
+      tn = min(tn, next_rel);
+    }
+    if (POL == POL_ISJL) {
+      if (planned > 0 && t_w1 > t) {
+        bool w0_wait = readlane(ws_end[0], 0) == IDLE &&
+                       ((uint32_t)readlane((int)ws_q[0], 0) & 0xFFFFu) != QNONE;
+        if (w0_wait) tn = min(tn, t_w1);
+      }
+      if (mode == 0 && kv_block && alpha != IDLE) tn = min(tn, S.min_s + alpha + 1);
+    }
+    if (tn == IDLE || tn <= t || ++iter > iter_max) {
+      failed = true;
+      break;
+    }
+
+    // (6) account steps t .. tn-1 (Section 5)
+    const int64_t D = (int64_t)(tn - t);
+    if (S.nact == 0) {
+      acc_C += a.c * D;
+      acc_W += a.c * D;
+    } else {
+      const int64_t s = S.nact;
+      const int64_t m0 = (int64_t)(t - S.min_s) + 1;
+      const int64_t sm = D * m0 + D * (D - 1) / 2;
+      acc_E += D * (S.sum_s - s * (int64_t)S.min_s);
+      acc_C += a.c * D + a.tau * s * sm;
+      acc_W += a.c * D + a.tau * sm;
+      const int ext = S.max_s - S.min_s;
+      acc_ext += D * ext;
+      acc_busy += D;
+      if (ext > alpha) acc_unfair += D;
+      acc_maxext = max(acc_maxext, ext);
+      acc_maxact = max(acc_maxact, S.nact);
+      acc_peak = max(acc_peak, s * (int64_t)tn - S.sum_s);
+    }
+    S.t = tn;
+  }
+
+  if (failed) {
+    write_marker(a.out, inst, T_INTERNAL, lane);
+    return;
+  }
+  if (lane == 0) {
+    fsched_metrics m;
+    m.T = S.t;
+    m.O = osum;
+    m.Q = qsum;
+    m.E = acc_E;
+    m.C = acc_C;
+    m.W = acc_W;
+    m.sum_completion = S.sum_comp;
+    m.sum_latency = S.sum_comp - rsum;
+    m.sum_extent = acc_ext;
+    m.busy_steps = acc_busy;
+    m.peak_kv = acc_peak;
+    m.unfair_steps = acc_unfair;
+    m.max_extent = acc_maxext;
+    m.max_active = acc_maxact;
+    a.out[inst] = m;
+  }
+}
+
+template <int POL>
+hipError_t launch_sim(const SimArgs& a, int K, int NW, bool general, int wpb, size_t lds,
+                      hipStream_t s) {
+  const int64_t blocks = (a.n_inst + wpb - 1) / wpb;
+  dim3 grid((unsigned)blocks), block((unsigned)(wpb * WAVE));
+#define FS_LAUNCH(KK, NN, GG)                                                        \
+  if (K == KK && NW == NN && general == GG) {                                        \
+    hipLaunchKernelGGL((simulate_kernel<POL, KK, NN, GG>), grid, block, lds, s, a);  \
+    return hipGetLastError();                                                        \
+  }
+#define FS_LAUNCH_K(KK) \
+  FS_LAUNCH(KK, 1, false) FS_LAUNCH(KK, 2, false) FS_LAUNCH(KK, 1, true) FS_LAUNCH(KK, 2, true)
+  FS_LAUNCH_K(1)
+  FS_LAUNCH_K(2)
+  FS_LAUNCH_K(4)
+  FS_LAUNCH_K(8)
+  FS_LAUNCH_K(16)
+#undef FS_LAUNCH_K
+#undef FS_LAUNCH
+  return hipErrorInvalidValue;
+}
+
+}  // namespace fs

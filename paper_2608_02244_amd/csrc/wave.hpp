@@ -1,0 +1,126 @@
+// Wavefront (64-lane) primitives for gfx950: DPP reductions and scans,
+// ballot helpers and LDS ordering within one wave.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fs {
+
+constexpr int WAVE = 64;
+
+__device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return (uint64_t)__ballot(p); }
+
+// Number of set bits of `mask` below the calling lane.
+__device__ __forceinline__ int mbcnt(uint64_t mask) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                        __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+__device__ __forceinline__ int readlane(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ uint32_t uniu(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
+}
+__device__ __forceinline__ int64_t uni64(int64_t v) {
+  uint32_t lo = uniu((uint32_t)v), hi = uniu((uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ int first_lane(uint64_t m) { return m ? __builtin_ctzll(m) : -1; }
+
+// DPP move with a compile-time control word.
+template <int CTRL, int ROW_MASK = 0xf, int BANK_MASK = 0xf, bool BOUND = false>
+__device__ __forceinline__ int dpp(int old, int src) {
+  return __builtin_amdgcn_update_dpp(old, src, CTRL, ROW_MASK, BANK_MASK, BOUND);
+}
+
+// quad_perm [1,0,3,2], [2,3,0,1]; row_half_mirror; row_mirror; row_bcast15; row_bcast31
+enum : int {
+  DPP_QP_XOR1 = 0xB1,
+  DPP_QP_XOR2 = 0x4E,
+  DPP_HALF_MIRROR = 0x141,
+  DPP_MIRROR = 0x140,
+  DPP_BCAST15 = 0x142,
+  DPP_BCAST31 = 0x143,
+  DPP_ROW_SHR1 = 0x111,
+  DPP_ROW_SHR2 = 0x112,
+  DPP_ROW_SHR3 = 0x113,
+  DPP_ROW_SHR4 = 0x114,
+  DPP_ROW_SHR8 = 0x118,
+};
+
+// Reductions: after the butterfly inside each row of 16 every lane holds its
+// row's value; the two broadcasts fold rows 0..3 into lanes 48..63.
+__device__ __forceinline__ int wave_min(int v) {
+  v = min(v, dpp<DPP_QP_XOR1>(v, v));
+  v = min(v, dpp<DPP_QP_XOR2>(v, v));
+  v = min(v, dpp<DPP_HALF_MIRROR>(v, v));
+  v = min(v, dpp<DPP_MIRROR>(v, v));
+  v = min(v, dpp<DPP_BCAST15, 0xa>(v, v));
+  v = min(v, dpp<DPP_BCAST31, 0xc>(v, v));
+  return readlane(v, 63);
+}
+
+__device__ __forceinline__ int wave_max(int v) {
+  v = max(v, dpp<DPP_QP_XOR1>(v, v));
+  v = max(v, dpp<DPP_QP_XOR2>(v, v));
+  v = max(v, dpp<DPP_HALF_MIRROR>(v, v));
+  v = max(v, dpp<DPP_MIRROR>(v, v));
+  v = max(v, dpp<DPP_BCAST15, 0xa>(v, v));
+  v = max(v, dpp<DPP_BCAST31, 0xc>(v, v));
+  return readlane(v, 63);
+}
+
+__device__ __forceinline__ uint32_t wave_umin(uint32_t v) {
+  int x = (int)v;
+  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_QP_XOR1>(x, x));
+  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_QP_XOR2>(x, x));
+  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_HALF_MIRROR>(x, x));
+  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_MIRROR>(x, x));
+  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_BCAST15, 0xa>(x, x));
+  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_BCAST31, 0xc>(x, x));
+  return (uint32_t)readlane(x, 63);
+}
+
+// Sum of int32 values (the caller guarantees the total fits).
+__device__ __forceinline__ int wave_sum(int v) {
+  v += dpp<DPP_QP_XOR1>(0, v);
+  v += dpp<DPP_QP_XOR2>(0, v);
+  v += dpp<DPP_HALF_MIRROR>(0, v);
+  v += dpp<DPP_MIRROR>(0, v);
+  v += dpp<DPP_BCAST15, 0xa>(0, v);
+  v += dpp<DPP_BCAST31, 0xc>(0, v);
+  return readlane(v, 63);
+}
+
+// Inclusive prefix sum over lanes 0..63.
+__device__ __forceinline__ int wave_scan_incl(int x) {
+  int v = x;
+  v += dpp<DPP_ROW_SHR1, 0xf, 0xf, true>(0, x);
+  v += dpp<DPP_ROW_SHR2, 0xf, 0xf, true>(0, x);
+  v += dpp<DPP_ROW_SHR3, 0xf, 0xf, true>(0, x);
+  v += dpp<DPP_ROW_SHR4, 0xf, 0xe, false>(0, v);
+  v += dpp<DPP_ROW_SHR8, 0xf, 0xc, false>(0, v);
+  v += dpp<DPP_BCAST15, 0xa, 0xf, false>(0, v);
+  v += dpp<DPP_BCAST31, 0xc, 0xf, false>(0, v);
+  return v;
+}
+
+// 64-bit sum through cross-lane shuffles (used outside the hot loop).
+__device__ __forceinline__ int64_t wave_sum64(int64_t v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+  return uni64(v);
+}
+
+// Order LDS accesses of this wave: all lanes of a wave issue LDS operations in
+// program order; this keeps the compiler from moving memory operations across
+// a cross-lane hand-off and waits for outstanding LDS traffic.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+}  // namespace fs

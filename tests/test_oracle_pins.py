@@ -280,8 +280,19 @@ def batch_grouping_bruteforce(lengths, B):
 
 def test_alpha_zero_is_ljf_and_optimal():
     """alpha = 0 is LJF's endpoint (Corollary on certified profit): ISJL produces
-    LJF's schedule, and the optimum equals the best grouping into batches."""
+    LJF's schedule (also with releases and a KV budget), and offline the optimum
+    equals the best grouping into batches."""
     rng = np.random.default_rng(11)
+    for trial in range(60):
+        n = int(rng.integers(1, 16))
+        B = int(rng.integers(1, 6))
+        a, p, o = random_tables(rng, 1, n, 5, 12, max_arrival=int(rng.choice([0, 8, 40])))
+        M_kv = int(rng.choice([0, 15, 30]))
+        _, si, _ = oracle.simulate(a, p, o, policy="isjl", B=B, alpha=0, M_kv=M_kv,
+                                   schedule=True)
+        _, sl, _ = oracle.simulate(a, p, o, policy="ljf", B=B, alpha=0, M_kv=M_kv,
+                                   schedule=True)
+        assert (si == sl).all()
     for trial in range(60):
         n = int(rng.integers(1, 8))
         B = int(rng.integers(1, 4))
