@@ -593,7 +593,8 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
                   hi = r + L1 * s;
                   lo = L1 > 0 ? r + (L1 - 1) * s + 1 : r;
                 } else {
-                  lo = r + 63 * s + 1;
+                  // after the last probe inside [r, n)
+                  lo = r + ((span - 1) / s) * s + 1;
                   hi = n;
                 }
                 int q = lo + lane;

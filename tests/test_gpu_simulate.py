@@ -46,7 +46,29 @@ def gpu_sim(dev, a, p, o, schedule=True, **kw):
     return m, None, None
 
 
+def first_divergence(gs, rs):
+    """Instance and job of the earliest start at which two schedules differ."""
+    rows = np.nonzero((gs != rs).any(1))[0]
+    if len(rows) == 0:
+        return None
+    i = rows[0]
+    js = np.nonzero(gs[i] != rs[i])[0]
+    j = js[np.argmin(np.minimum(gs[i, js], rs[i, js]))]
+    return int(i), int(j)
+
+
 def assert_same(ctx, got, ref, gs=None, rs=None, gf=None, rf=None):
+    if gs is not None:
+        d = first_divergence(gs, rs)
+        if d is not None:
+            i, j = d
+            t0 = min(gs[i, j], rs[i, j])
+            near = np.nonzero((np.abs(rs[i] - t0) <= 3) | (np.abs(gs[i] - t0) <= 3))[0]
+            raise AssertionError(
+                f"{ctx}: schedules diverge at instance {i}, job {j} (gpu start {gs[i, j]}, "
+                f"oracle start {rs[i, j]}, len {rf[i, j] - rs[i, j]}); jobs starting near "
+                f"{t0}: " + "; ".join(f"job {k} len {rf[i, k] - rs[i, k]} gpu {gs[i, k]} "
+                                      f"oracle {rs[i, k]}" for k in near[:12]))
     for f in fs.METRIC_FIELDS:
         if not np.array_equal(got[f], ref[f]):
             bad = np.nonzero(got[f] != ref[f])[0][:5]
