@@ -1,0 +1,145 @@
+"""Benchmark: ISJL instance-steps per second on one MI355X.
+
+One step = one fsched_simulate call over the whole batch of the headline
+workload (65,536 instances x 2,000 jobs, heavy-tailed outputs, Poisson
+arrivals, B = 512, M_kv = 1,048,576, alpha = 128, affine integer step cost):
+ordering, event loop, admissions, Section 5 accounting and the per-instance
+metrics, with the job tables already resident in HBM.  An instance-step is one
+logical step of one instance, so a step contributes sum_i T_i instance-steps.
+
+Prints one JSON line (see the design doc for the roofline definition).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "instance-steps/sec (ISJL, 1 MI355X) + fraction of gfx950 VALU/LDS/HBM roofline"
+UNIT = "instance-steps/s"
+# gfx950: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = int32 VALU lane operations per second
+PEAK_ALU = 256 * 64 * 2.4e9
+
+
+def algorithmic_ops(n_inst: int, n: int, B: int, policy: str, sorted_arrivals: bool) -> float:
+    """Lane operations the event-driven method needs per launch (roofline):
+    ordering by a bitonic network (2 per compare-exchange), and per job one
+    admission and one completion, each scanning the B-slot active table once
+    (B compares) plus the table reductions after the completion (B), and one rank
+    lookup (ceil(log2 n) + 1 compares)."""
+    NP = 64
+    while NP < n:
+        NP *= 2
+    L = NP.bit_length() - 1
+    sort_ce = (NP // 2) * L * (L + 1) // 2
+    needs_sort = policy != "fcfs" or not sorted_arrivals
+    per_inst = (2 * sort_ce if needs_sort else 0) + n * (3 * min(B, n) + L + 1)
+    return float(n_inst) * per_inst
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="pareto_65536x2000")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the instances are "
+              "independent, so more GPUs would each take a contiguous share of them "
+              "(see DESIGN.md), but this build measures one GPU.", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+    import workload
+    import paper_2608_02244_amd as fs
+
+    w = workload.WORKLOADS[args.workload]
+    alpha = w.alphas[0]
+    policy = "isjl"
+    dev = torch.device("cuda:0")
+    t0 = time.perf_counter()
+    a, p, o = workload.generate(w)
+    gen_s = time.perf_counter() - t0
+    sorted_arrivals = bool((np.diff(a, axis=1) >= 0).all())
+    ta, tp, to = (torch.from_numpy(x).to(dev) for x in (a, p, o))
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    kw = dict(policy=policy, B=w.B, alpha=alpha, M_kv=w.M_kv, cost_c=w.cost_c,
+              cost_tau=w.cost_tau)
+
+    raw, _, _ = fs.simulate(ta, tp, to, **kw)
+    torch.cuda.synchronize()
+    m = fs.metrics_view(raw)
+    if (m["T"] < 0).any():
+        raise RuntimeError("some instance reported an error marker")
+    inst_steps = int(m["T"].sum())
+
+    for _ in range(args.warmup):
+        fs.simulate(ta, tp, to, **kw)
+    torch.cuda.synchronize()
+    ev_start = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ev_end = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for k in range(args.steps):
+        ev_start[k].record(stream)
+        fs.simulate(ta, tp, to, **kw)
+        ev_end[k].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    launch_ms = [s.elapsed_time(e) for s, e in zip(ev_start, ev_end)]
+    avg_launch_s = sum(launch_ms) / len(launch_ms) / 1e3
+    ms_per_step = wall / args.steps * 1e3
+    value = inst_steps * args.steps / wall
+
+    ops = algorithmic_ops(w.n_inst, w.n_jobs, w.B, policy, sorted_arrivals)
+    achieved = ops / avg_launch_s
+    roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_ALU / 1e12,
+                "unit": "Tops/s (int32 lane operations)", "frac": achieved / PEAK_ALU,
+                "traffic": None, "kernel": f"simulate_kernel<ISJL> ({w.n_inst} waves)",
+                "avg_launch_ms": avg_launch_s * 1e3, "ops_per_launch": ops}
+
+    out = {"metric": METRIC, "value": value, "unit": UNIT, "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
+           "config": {"workload": w.name, "policy": policy, "n_inst": w.n_inst,
+                      "n_jobs": w.n_jobs, "B": w.B, "alpha": alpha, "M_kv": w.M_kv,
+                      "cost_c": w.cost_c, "cost_tau": w.cost_tau,
+                      "instance_steps_per_step": inst_steps, "generate_s": round(gen_s, 3)},
+           "roofline": roofline}
+
+    if not args.no_cpu_baseline:
+        import oracle
+        kw_o = dict(policy=policy, B=w.B, alpha=alpha, M_kv=w.M_kv, cost_c=w.cost_c,
+                    cost_tau=w.cost_tau)
+        c0 = time.perf_counter()
+        oracle.simulate(a[:1], p[:1], o[:1], **kw_o)
+        one = max(time.perf_counter() - c0, 1e-4)
+        k = int(max(1, min(w.n_inst, args.cpu_seconds / one)))
+        c0 = time.perf_counter()
+        ref = oracle.simulate(a[:k], p[:k], o[:k], **kw_o)
+        cpu_s = time.perf_counter() - c0
+        parity = all(np.array_equal(ref[f], m[f][:k]) for f in fs.METRIC_FIELDS)
+        out["cpu_baseline"] = {"value": float(ref["T"].sum()) / cpu_s, "unit": UNIT, "cores": 1,
+                               "kind": "oracle",
+                               "sample": f"first {k} of {w.n_inst} instances of {w.name} "
+                                         f"(ISJL alpha={alpha}), single-threaded C oracle, "
+                                         f"{cpu_s:.1f} s",
+                               "parity_on_sample": parity}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
