@@ -7,6 +7,7 @@
 
 #include "fsched.h"
 #include "sim_common.hpp"
+#include "dec_common.hpp"
 
 namespace {
 
@@ -202,17 +203,61 @@ int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs
                           const int32_t* arrival, const int32_t* prompt, const int32_t* output,
                           const int32_t* start, fsched_metrics* out, uint32_t* violation,
                           void* stream) {
-  (void)p;
-  (void)n_inst;
-  (void)n_jobs;
-  (void)arrival;
-  (void)prompt;
-  (void)output;
-  (void)start;
-  (void)out;
-  (void)violation;
-  (void)stream;
-  return FSCHED_ENOTIMPL;
+  int rc = check_params(p, false);
+  if (rc) return rc;
+  if (n_inst < 0 || n_jobs < 1) return FSCHED_EINVAL;
+  if (n_inst == 0) return FSCHED_OK;
+  if (!arrival || !prompt || !output || !start || !out || !violation) return FSCHED_EINVAL;
+  if (n_jobs > fs::DEC_MAX_JOBS) return FSCHED_ETOOLARGE;
+  hipStream_t s = (hipStream_t)stream;
+  fs::DecArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.n_inst = n_inst;
+  a.n = n_jobs;
+  a.B = p->B;
+  a.alpha = p->alpha;
+  a.M = p->M_kv;
+  a.c = p->cost_c;
+  a.tau = p->cost_tau;
+  a.NP2 = next_pow2(2 * n_jobs);
+  a.wave_words = a.NP2 + (n_jobs + 3) / 4;
+  a.wave_words = (a.wave_words + 3) & ~3;
+  const size_t per_wave = (size_t)a.wave_words * 4;
+  int wpb = 4;
+  while (wpb > 1 && per_wave * wpb > 64 * 1024) wpb >>= 1;
+  const size_t lds = per_wave * wpb;
+  if (p->flags & FSCHED_F_DEVICE_PTRS) {
+    a.arrival = arrival;
+    a.prompt = prompt;
+    a.output = output;
+    a.start = start;
+    a.out = out;
+    a.viol = violation;
+    hipError_t e = fs::launch_decompose(a, wpb, lds, s);
+    if (e != hipSuccess) return hip_fail(e);
+    if (p->flags & FSCHED_F_SYNC) {
+      e = hipStreamSynchronize(s);
+      if (e != hipSuccess) return hip_fail(e);
+    }
+    return FSCHED_OK;
+  }
+  const size_t tb = (size_t)n_inst * (size_t)n_jobs * sizeof(int32_t);
+  Staging st;
+  a.arrival = (const int32_t*)st.upload(arrival, tb);
+  a.prompt = (const int32_t*)st.upload(prompt, tb);
+  a.output = (const int32_t*)st.upload(output, tb);
+  a.start = (const int32_t*)st.upload(start, tb);
+  a.out = (fsched_metrics*)st.alloc((size_t)n_inst * sizeof(fsched_metrics));
+  a.viol = (uint32_t*)st.alloc((size_t)n_inst * sizeof(uint32_t));
+  if (st.err != hipSuccess) return hip_fail(st.err);
+  hipError_t e = fs::launch_decompose(a, wpb, lds, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e == hipSuccess)
+    e = hipMemcpy(out, a.out, (size_t)n_inst * sizeof(fsched_metrics), hipMemcpyDeviceToHost);
+  if (e == hipSuccess)
+    e = hipMemcpy(violation, a.viol, (size_t)n_inst * sizeof(uint32_t), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e);
+  return markers_to_code(out, n_inst);
 }
 
 int fsched_bruteforce_opt(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
