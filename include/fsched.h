@@ -172,11 +172,15 @@ int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs
  * integer program with release steps and M_kv added): the least makespan over
  * every start vector with s_i >= arrival_i, at most B active jobs per step,
  * reservations within M_kv unless a job runs alone, and |s_i - s_j| <= alpha for
- * every pair active at a common step.
- *   n_jobs     <= 8 (ETOOLARGE otherwise); every length <= 255.
+ * every pair active at a common step.  Exhaustive search over schedules in start
+ * order with a memo and lower bounds, started from the ISJL schedule of the
+ * instance (which is returned when nothing beats it).
+ *   n_jobs     <= 8 (ETOOLARGE otherwise); every length <= 255 and every
+ *              arrival <= 4095 (else T = FSCHED_T_TOOLARGE / ETOOLARGE).
  *   T_opt      [n_inst] int64 optimum makespan.
  *   start_opt  nullable [n_inst][n_jobs] int32: one optimal schedule.
- * p->policy, cost_c and cost_tau are ignored. */
+ * p->policy, p->flags other than DEVICE_PTRS / SYNC, cost_c and cost_tau are
+ * ignored. */
 int fsched_bruteforce_opt(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
                           const int32_t* arrival, const int32_t* prompt, const int32_t* output,
                           int64_t* T_opt, int32_t* start_opt, void* stream);

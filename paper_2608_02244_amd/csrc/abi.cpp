@@ -8,6 +8,7 @@
 #include "fsched.h"
 #include "sim_common.hpp"
 #include "dec_common.hpp"
+#include "opt_common.hpp"
 
 namespace {
 
@@ -86,7 +87,7 @@ struct Staging {
 
 int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int32_t* arrival,
                     const int32_t* prompt, const int32_t* output, fsched_metrics* out,
-                    int32_t* start, int32_t* finish, hipStream_t s) {
+                    int64_t* out_T, int32_t* start, int32_t* finish, hipStream_t s) {
   const int Beff = (p->B == 0 || p->B > n) ? n : p->B;
   if (n > fs::MAX_JOBS || Beff > fs::MAX_WORKERS) return FSCHED_ETOOLARGE;
   int K = 1;
@@ -112,6 +113,7 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
   a.prompt = prompt;
   a.output = output;
   a.out = out;
+  a.out_T = out_T;
   a.start = start;
   a.finish = finish;
 
@@ -170,7 +172,8 @@ int fsched_simulate(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
   if (!arrival || !prompt || !output || !out) return FSCHED_EINVAL;
   hipStream_t s = (hipStream_t)stream;
   if (p->flags & FSCHED_F_DEVICE_PTRS) {
-    rc = launch_simulate(p, n_inst, n_jobs, arrival, prompt, output, out, start, finish, s);
+    rc = launch_simulate(p, n_inst, n_jobs, arrival, prompt, output, out, nullptr, start, finish,
+                         s);
     if (rc) return rc;
     if (p->flags & FSCHED_F_SYNC) {
       hipError_t e = hipStreamSynchronize(s);
@@ -188,7 +191,7 @@ int fsched_simulate(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
   int32_t* dst = start ? (int32_t*)st.alloc(tb) : nullptr;
   int32_t* dfi = finish ? (int32_t*)st.alloc(tb) : nullptr;
   if (st.err != hipSuccess) return hip_fail(st.err);
-  rc = launch_simulate(p, n_inst, n_jobs, da, dp, dq, dout, dst, dfi, s);
+  rc = launch_simulate(p, n_inst, n_jobs, da, dp, dq, dout, nullptr, dst, dfi, s);
   if (rc) return rc;
   hipError_t e = hipStreamSynchronize(s);
   if (e == hipSuccess)
@@ -263,16 +266,71 @@ int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs
 int fsched_bruteforce_opt(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
                           const int32_t* arrival, const int32_t* prompt, const int32_t* output,
                           int64_t* T_opt, int32_t* start_opt, void* stream) {
-  (void)p;
-  (void)n_inst;
-  (void)n_jobs;
-  (void)arrival;
-  (void)prompt;
-  (void)output;
-  (void)T_opt;
-  (void)start_opt;
-  (void)stream;
-  return FSCHED_ENOTIMPL;
+  int rc = check_params(p, false);
+  if (rc) return rc;
+  if (n_inst < 0 || n_jobs < 1) return FSCHED_EINVAL;
+  if (n_jobs > fs::OPT_MAX_JOBS) return FSCHED_ETOOLARGE;
+  if (n_inst == 0) return FSCHED_OK;
+  if (!arrival || !prompt || !output || !T_opt) return FSCHED_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  // The ISJL makespan (and schedule) is the incumbent the exact search has to beat.
+  fsched_params sp = *p;
+  sp.policy = FSCHED_ISJL;
+  sp.flags = 0;
+  sp.cost_c = 0;
+  sp.cost_tau = 0;
+  fs::OptArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.n_inst = n_inst;
+  a.n = n_jobs;
+  a.B = (p->B == 0 || p->B > n_jobs) ? n_jobs : p->B;
+  a.alpha = p->alpha;
+  a.M = p->M_kv;
+  a.wave_words = (int32_t)fs::opt_lds_words_per_wave();
+  const int wpb = 2;
+  const size_t lds = (size_t)a.wave_words * 4 * wpb;
+  auto run = [&](const int32_t* da, const int32_t* dp, const int32_t* dq, int64_t* dT,
+                 int32_t* dS) -> int {
+    int r = launch_simulate(&sp, n_inst, n_jobs, da, dp, dq, nullptr, dT, dS, nullptr, s);
+    if (r) return r;
+    a.arrival = da;
+    a.prompt = dp;
+    a.output = dq;
+    a.T = dT;
+    a.start = dS;
+    hipError_t e = fs::launch_opt(a, wpb, lds, s);
+    return e == hipSuccess ? FSCHED_OK : hip_fail(e);
+  };
+  if (p->flags & FSCHED_F_DEVICE_PTRS) {
+    rc = run(arrival, prompt, output, T_opt, start_opt);
+    if (rc) return rc;
+    if (p->flags & FSCHED_F_SYNC) {
+      hipError_t e = hipStreamSynchronize(s);
+      if (e != hipSuccess) return hip_fail(e);
+    }
+    return FSCHED_OK;
+  }
+  const size_t tb = (size_t)n_inst * (size_t)n_jobs * sizeof(int32_t);
+  Staging st;
+  const int32_t* da = (const int32_t*)st.upload(arrival, tb);
+  const int32_t* dp = (const int32_t*)st.upload(prompt, tb);
+  const int32_t* dq = (const int32_t*)st.upload(output, tb);
+  int64_t* dT = (int64_t*)st.alloc((size_t)n_inst * sizeof(int64_t));
+  int32_t* dS = start_opt ? (int32_t*)st.alloc(tb) : nullptr;
+  if (st.err != hipSuccess) return hip_fail(st.err);
+  rc = run(da, dp, dq, dT, dS);
+  if (rc) return rc;
+  hipError_t e = hipStreamSynchronize(s);
+  if (e == hipSuccess)
+    e = hipMemcpy(T_opt, dT, (size_t)n_inst * sizeof(int64_t), hipMemcpyDeviceToHost);
+  if (e == hipSuccess && start_opt) e = hipMemcpy(start_opt, dS, tb, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e);
+  for (int64_t i = 0; i < n_inst; ++i) {
+    if (T_opt[i] == FSCHED_T_INVALID) return FSCHED_EINVAL;
+    if (T_opt[i] == FSCHED_T_INTERNAL) rc = FSCHED_EINTERNAL;
+    else if (T_opt[i] < 0) rc = (T_opt[i] == FSCHED_T_RANGE) ? FSCHED_ERANGE : FSCHED_ETOOLARGE;
+  }
+  return rc;
 }
 
 }  // extern "C"

@@ -34,7 +34,8 @@ struct SimArgs {
   const int32_t* arrival;
   const int32_t* prompt;
   const int32_t* output;
-  fsched_metrics* out;
+  fsched_metrics* out;  // per-instance metrics, or
+  int64_t* out_T;       // when non-null: only the makespan (or marker) per instance
   int32_t* start;
   int32_t* finish;
 };

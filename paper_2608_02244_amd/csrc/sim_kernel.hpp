@@ -64,8 +64,11 @@ __device__ inline void wave_bitonic_sort(uint32_t* W, int NP, int lane) {
   }
 }
 
-__device__ inline void write_marker(fsched_metrics* out, int64_t inst, int64_t code, int lane) {
-  if (lane == 0) {
+__device__ inline void write_marker(fsched_metrics* out, int64_t* out_T, int64_t inst,
+                                    int64_t code, int lane) {
+  if (lane == 0 && out_T) {
+    out_T[inst] = code;
+  } else if (lane == 0) {
     fsched_metrics m;
     m.T = code;
     m.O = m.Q = m.E = m.C = m.W = 0;
@@ -168,8 +171,9 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
   const int32_t* P = a.prompt + row;
   const int32_t* O = a.output + row;
 
-  if (GEN) {
-    if (a.out[inst].T != T_DEFERRED) return;  // the sorted-arrival kernel handled it
+  if (GEN) {  // only instances the sorted-arrival kernel deferred
+    const int64_t prev = a.out_T ? a.out_T[inst] : a.out[inst].T;
+    if (prev != T_DEFERRED) return;
   }
 
   // ---- load, validate, instance constants --------------------------------
@@ -191,15 +195,15 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
   big = ballot(big != 0) != 0;
   unsorted = ballot(unsorted != 0) != 0;
   if (bad) {
-    write_marker(a.out, inst, FSCHED_T_INVALID, lane);
+    write_marker(a.out, a.out_T, inst, FSCHED_T_INVALID, lane);
     return;
   }
   if (big) {
-    write_marker(a.out, inst, FSCHED_T_TOOLARGE, lane);
+    write_marker(a.out, a.out_T, inst, FSCHED_T_TOOLARGE, lane);
     return;
   }
   if (!GEN && unsorted) {
-    write_marker(a.out, inst, T_DEFERRED, lane);
+    write_marker(a.out, a.out_T, inst, T_DEFERRED, lane);
     return;
   }
   maxlen = wave_max(maxlen);
@@ -208,7 +212,7 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
   qsum = wave_sum64(qsum);
   rsum = wave_sum64(rsum);
   if (GEN && maxarr >= ARR_LIMIT) {
-    write_marker(a.out, inst, FSCHED_T_TOOLARGE, lane);
+    write_marker(a.out, a.out_T, inst, FSCHED_T_TOOLARGE, lane);
     return;
   }
   {
@@ -217,13 +221,13 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
     double amin = a.alpha < maxlen ? (double)a.alpha : (double)maxlen;
     double tb = (double)maxarr + (double)osum + (double)n * amin + 1.0;
     if (tb >= 2147483000.0) {
-      write_marker(a.out, inst, FSCHED_T_TOOLARGE, lane);
+      write_marker(a.out, a.out_T, inst, FSCHED_T_TOOLARGE, lane);
       return;
     }
     double cb = (double)a.c * tb + (double)a.tau * (double)osum * (double)maxlen;
     double wb = (double)a.c * tb + (double)a.tau * tb * (double)maxlen;
     if (cb > 4.0e18 || wb > 4.0e18) {
-      write_marker(a.out, inst, FSCHED_T_RANGE, lane);
+      write_marker(a.out, a.out_T, inst, FSCHED_T_RANGE, lane);
       return;
     }
   }
@@ -833,10 +837,12 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
   }
 
   if (failed) {
-    write_marker(a.out, inst, T_INTERNAL, lane);
+    write_marker(a.out, a.out_T, inst, T_INTERNAL, lane);
     return;
   }
-  if (lane == 0) {
+  if (lane == 0 && a.out_T) {
+    a.out_T[inst] = S.t;
+  } else if (lane == 0) {
     fsched_metrics m;
     m.T = S.t;
     m.O = osum;
