@@ -287,7 +287,7 @@ int fsched_bruteforce_opt(const fsched_params* p, int64_t n_inst, int32_t n_jobs
   a.alpha = p->alpha;
   a.M = p->M_kv;
   a.wave_words = (int32_t)fs::opt_lds_words_per_wave();
-  const int wpb = 2;
+  const int wpb = 1;
   const size_t lds = (size_t)a.wave_words * 4 * wpb;
   auto run = [&](const int32_t* da, const int32_t* dp, const int32_t* dq, int64_t* dT,
                  int32_t* dS) -> int {

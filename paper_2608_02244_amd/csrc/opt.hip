@@ -37,7 +37,9 @@ namespace fs {
 namespace {
 
 constexpr int NMAX = 8;
-constexpr int MEMO = 1024;            // memo entries per wave (power of two)
+constexpr int MEMO_BYTES = 32768;     // memo bytes per wave
+constexpr int MEMO_W = MEMO_BYTES / 16;  // general layout: 4 words per entry
+constexpr int MEMO_C = MEMO_BYTES / 8;   // compact layout: one 64-bit word per entry
 constexpr int FRAMES = NMAX + 2;      // DFS depth <= n, plus the root
 constexpr int FW = 8;                 // words per frame
 constexpr int CACHE = 192;            // cached candidate keys per frame (3 per lane)
@@ -53,7 +55,9 @@ struct Inst {
   int64_t M;
   int len[NMAX], arr[NMAX];
   uint32_t eqprev[NMAX];
+  uint32_t compat[NMAX];  // jobs that may run beside job j under the KV budget
   uint32_t full;
+  bool compact;           // B <= 3 and every arrival 0: 64-bit memo entries
 };
 
 __device__ __forceinline__ int prog_of(uint32_t plo, uint32_t phi, int j) {
@@ -97,11 +101,31 @@ __device__ inline uint32_t cand_key(const Inst& I, uint32_t S, int sig, uint32_t
   if (I.M != 0 && cnt > 0 && sumlen + lk > I.M) return NOKEY;
   const int sig2 = sig + d;
   int maxu = 0;
+  uint32_t R = 0;  // jobs with work left after the start of k
 #pragma unroll
-  for (int j = 0; j < NMAX; ++j)
-    if (j < I.n && j != k && !((S >> j) & 1u)) maxu = max(maxu, max(0, I.arr[j] - sig2) + I.len[j]);
+  for (int j = 0; j < NMAX; ++j) {
+    if (j < I.n && j != k && !((S >> j) & 1u)) {
+      maxu = max(maxu, max(0, I.arr[j] - sig2) + I.len[j]);
+      R |= 1u << j;
+    }
+    const int p = prog_of(plo, phi, j);
+    if (p != 0xFF && I.len[j] - p > d) R |= 1u << j;
+  }
+  R |= 1u << k;
+  // A job that fits beside no other remaining job (KV budget, or B = 1) runs
+  // alone: its remaining steps are serial with everything else.
+  int alone = 0;
+#pragma unroll
+  for (int j = 0; j < NMAX; ++j) {
+    if (((R >> j) & 1u) && (I.compat[j] & R & ~(1u << j)) == 0u) {
+      const int p = prog_of(plo, phi, j);
+      int rj = I.len[j];
+      if (j != k && p != 0xFF) rj = I.len[j] - p - d;
+      alone += rj;
+    }
+  }
   const int work = sumrem + sumU - lk;
-  const int lb = max(max(maxrem, maxu), (work + I.B - 1) / I.B);
+  const int lb = max(max(maxrem, maxu), alone + (work - alone + I.B - 1) / I.B);
   return ((uint32_t)(d + lb) << 16) | ((uint32_t)d << 3) | (uint32_t)k;
 }
 
@@ -114,50 +138,106 @@ __device__ __forceinline__ uint32_t mix(uint32_t k0, uint32_t k1, uint32_t k2) {
 }
 
 struct Memo {
-  uint32_t* k0;
-  uint32_t* k1;
-  uint32_t* k2;
-  uint32_t* val;  // value | exact << 31
-};
+  uint32_t* base;
+  bool compact;
 
-// returns value | exact << 31, or NOKEY if absent
-__device__ inline uint32_t memo_get(const Memo& m, uint32_t a, uint32_t b, uint32_t c, int lane) {
-  const uint32_t h = mix(a, b, c);
-  const int slot = (int)((h + (uint32_t)lane) & (MEMO - 1));
-  const uint32_t x = m.k0[slot];
-  const bool hit = x == a && m.k1[slot] == b && m.k2[slot] == c;
-  const bool empty = x == 0u;
-  const uint64_t mh = ballot(hit), me = ballot(empty);
-  if (!mh) return NOKEY;
-  const int L = __builtin_ctzll(mh);
-  if (me && __builtin_ctzll(me) < L) return NOKEY;  // not reachable: keys sit before any hole
-  return (uint32_t)readlane((int)m.val[slot], L);
-}
-
-__device__ inline void memo_put(const Memo& m, uint32_t a, uint32_t b, uint32_t c, uint32_t v,
-                                int lane) {
-  const uint32_t h = mix(a, b, c);
-  const int slot = (int)((h + (uint32_t)lane) & (MEMO - 1));
-  const uint32_t x = m.k0[slot];
-  const bool hit = x == a && m.k1[slot] == b && m.k2[slot] == c;
-  const bool empty = x == 0u;
-  const uint64_t mh = ballot(hit), me = ballot(empty);
-  int L;
-  if (mh) L = __builtin_ctzll(mh);
-  else if (me) L = __builtin_ctzll(me);
-  else L = 0;  // table full along this probe window: replace the home slot
-  if (lane == L) {
-    m.k0[slot] = a;
-    m.k1[slot] = b;
-    m.k2[slot] = c;
-    m.val[slot] = v;
+  // Compact key: valid | S | up to three active (index, progress) pairs in index order.
+  __device__ static uint64_t ckey(uint32_t S, uint32_t plo, uint32_t phi) {
+    uint64_t slots = 0;
+    int c = 0;
+#pragma unroll
+    for (int j = 0; j < NMAX; ++j) {
+      const int p = prog_of(plo, phi, j);
+      if (p != 0xFF && c < 3) {
+        slots |= (uint64_t)((j << 8) | p) << (11 * c);
+        c++;
+      }
+    }
+    for (int q = c; q < 3; ++q) slots |= (uint64_t)0x7FFu << (11 * q);
+    return (1ull << 63) | ((uint64_t)S << 55) | (slots << 16);
   }
-  wave_lds_sync();
-}
+
+  // value | exact << 31, or NOKEY if absent
+  __device__ uint32_t get(uint32_t a, uint32_t b, uint32_t c, uint32_t S, int lane) const {
+    if (compact) {
+      const uint64_t key = ckey(S, b, c);
+      const uint64_t* T = (const uint64_t*)base;
+      const uint32_t h = mix((uint32_t)(key >> 32), (uint32_t)key, 0u);
+      const int slot = (int)((h + (uint32_t)lane) & (MEMO_C - 1));
+      const uint64_t x = T[slot];
+      const bool hit = (x >> 16) == (key >> 16);
+      const bool empty = x == 0ull;
+      const uint64_t mh = ballot(hit), me = ballot(empty);
+      if (!mh) return NOKEY;
+      const int L = __builtin_ctzll(mh);
+      if (me && __builtin_ctzll(me) < L) return NOKEY;
+      const uint32_t v = (uint32_t)readlane((int)(uint32_t)(x & 0xFFFFu), L);
+      return (v & 0x7FFFu) | ((v & 0x8000u) << 16);
+    }
+    uint32_t* k0 = base;
+    uint32_t* k1 = base + MEMO_W;
+    uint32_t* k2 = base + 2 * MEMO_W;
+    uint32_t* val = base + 3 * MEMO_W;
+    const uint32_t h = mix(a, b, c);
+    const int slot = (int)((h + (uint32_t)lane) & (MEMO_W - 1));
+    const uint32_t x = k0[slot];
+    const bool hit = x == a && k1[slot] == b && k2[slot] == c;
+    const bool empty = x == 0u;
+    const uint64_t mh = ballot(hit), me = ballot(empty);
+    if (!mh) return NOKEY;
+    const int L = __builtin_ctzll(mh);
+    if (me && __builtin_ctzll(me) < L) return NOKEY;  // keys sit before any hole
+    return (uint32_t)readlane((int)val[slot], L);
+  }
+
+  __device__ void put(uint32_t a, uint32_t b, uint32_t c, uint32_t S, uint32_t v, int lane) {
+    if (compact) {
+      const uint64_t key = ckey(S, b, c);
+      uint64_t* T = (uint64_t*)base;
+      const uint32_t h = mix((uint32_t)(key >> 32), (uint32_t)key, 0u);
+      const int slot = (int)((h + (uint32_t)lane) & (MEMO_C - 1));
+      const uint64_t x = T[slot];
+      const bool hit = (x >> 16) == (key >> 16);
+      const bool empty = x == 0ull;
+      const uint64_t mh = ballot(hit), me = ballot(empty);
+      const int L = mh ? __builtin_ctzll(mh) : (me ? __builtin_ctzll(me) : 0);
+      const uint64_t e = key | (uint64_t)((v & 0x7FFFu) | ((v >> 16) & 0x8000u));
+      if (lane == L) T[slot] = e;
+      wave_lds_sync();
+      return;
+    }
+    uint32_t* k0 = base;
+    uint32_t* k1 = base + MEMO_W;
+    uint32_t* k2 = base + 2 * MEMO_W;
+    uint32_t* val = base + 3 * MEMO_W;
+    const uint32_t h = mix(a, b, c);
+    const int slot = (int)((h + (uint32_t)lane) & (MEMO_W - 1));
+    const uint32_t x = k0[slot];
+    const bool hit = x == a && k1[slot] == b && k2[slot] == c;
+    const bool empty = x == 0u;
+    const uint64_t mh = ballot(hit), me = ballot(empty);
+    int L;
+    if (mh) L = __builtin_ctzll(mh);
+    else if (me) L = __builtin_ctzll(me);
+    else L = 0;  // probe window full: replace the home slot
+    if (lane == L) {
+      k0[slot] = a;
+      k1[slot] = b;
+      k2[slot] = c;
+      val[slot] = v;
+    }
+    wave_lds_sync();
+  }
+
+  __device__ void clear(int lane) {
+    for (int i = lane; i < MEMO_BYTES / 4; i += WAVE) base[i] = 0u;
+    wave_lds_sync();
+  }
+};
 
 struct Dfs {
   const Inst& I;
-  const Memo& memo;
+  Memo& memo;
   uint32_t* F;      // FRAMES * FW words
   uint32_t* keys;   // FRAMES * CACHE candidate keys
   int lane;
@@ -237,7 +317,7 @@ struct Dfs {
           }
           ret = mr;
         } else {
-          const uint32_t v = memo_get(memo, ka, plo, phi, lane);
+          const uint32_t v = memo.get(ka, plo, phi, S, lane);
           if (v != NOKEY && ((v >> 31) || (int)(v & 0x7FFFFFFFu) >= bound)) {
             ret = (int)(v & 0x7FFFFFFFu);
           } else {
@@ -286,7 +366,7 @@ struct Dfs {
           if (++guard > GUARD) return -1;  // far above any search seen for n <= 8
           continue;
         }
-        memo_put(memo, ka, plo, phi, (uint32_t)best | ((best < bound) ? 0x80000000u : 0u), lane);
+        memo.put(ka, plo, phi, S, (uint32_t)best | ((best < bound) ? 0x80000000u : 0u), lane);
         ret = best;
       }
       if (depth == 0) return ret;
@@ -309,8 +389,7 @@ __global__ __launch_bounds__(256) void opt_kernel(OptArgs a) {
   if (inst >= a.n_inst) return;
   const int lane = lane_id();
   uint32_t* base = lds_raw + (size_t)wib * (size_t)a.wave_words;
-  Memo memo{base, base + MEMO, base + 2 * MEMO, base + 3 * MEMO};
-  uint32_t* frames = base + 4 * MEMO;
+  uint32_t* frames = base + MEMO_BYTES / 4;
   uint32_t* keys = frames + FRAMES * FW;
 
   const int n = a.n;
@@ -348,9 +427,19 @@ __global__ __launch_bounds__(256) void opt_kernel(OptArgs a) {
     I.eqprev[k] = e;
   }
   I.full = (n >= 32) ? 0xFFFFFFFFu : ((1u << n) - 1u);
-
-  for (int i = lane; i < MEMO; i += WAVE) memo.k0[i] = 0u;
-  wave_lds_sync();
+#pragma unroll
+  for (int j = 0; j < NMAX; ++j) {
+    uint32_t c = 0;
+#pragma unroll
+    for (int i = 0; i < NMAX; ++i)
+      if (i != j && i < n && j < n && I.B > 1 &&
+          (I.M == 0 || (int64_t)I.len[i] + I.len[j] <= I.M))
+        c |= 1u << i;
+    I.compat[j] = c;
+  }
+  I.compact = I.B <= 3 && I.rmax == 0;
+  Memo memo{base, I.compact};
+  memo.clear(lane);
 
   Dfs dfs{I, memo, frames, keys, lane};
   const uint32_t none = 0xFFFFFFFFu;
@@ -413,6 +502,6 @@ hipError_t launch_opt(const OptArgs& a, int wpb, size_t lds, hipStream_t s) {
   return hipGetLastError();
 }
 
-size_t opt_lds_words_per_wave() { return 4 * MEMO + FRAMES * FW + FRAMES * CACHE; }
+size_t opt_lds_words_per_wave() { return MEMO_BYTES / 4 + FRAMES * FW + FRAMES * CACHE; }
 
 }  // namespace fs
