@@ -52,6 +52,10 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--mode", default="simulate", choices=["simulate", "copy", "decompose", "opt"],
+                    help="simulate: the benchmark line; copy: a plain device copy of known size "
+                         "(calibrates the HBM byte counters); decompose / opt: time the other "
+                         "two library calls (for profiles)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the instances are "
@@ -64,6 +68,12 @@ def main() -> int:
     import workload
     import paper_2608_02244_amd as fs
 
+    if args.mode == "copy":
+        return copy_calibration(torch, args.steps)
+    if args.mode == "decompose":
+        return time_decompose(torch, np, workload, fs, args)
+    if args.mode == "opt":
+        return time_opt(torch, np, workload, fs, args)
     w = workload.WORKLOADS[args.workload]
     alpha = w.alphas[0]
     policy = "isjl"
@@ -138,6 +148,63 @@ def main() -> int:
                                          f"{cpu_s:.1f} s",
                                "parity_on_sample": parity}
     print(json.dumps(out), flush=True)
+    return 0
+
+
+def copy_calibration(torch, steps: int) -> int:
+    """A plain device-to-device copy of 1 GiB: 1 GiB read and 1 GiB written per
+    dispatch, the reference for the FETCH_SIZE / WRITE_SIZE counters."""
+    n = 1 << 28
+    x = torch.arange(n, dtype=torch.int32, device="cuda:0")
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    for _ in range(max(1, steps)):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"mode": "copy", "bytes_read_per_dispatch": 4 * n,
+                      "bytes_written_per_dispatch": 4 * n, "dispatches": max(1, steps)}))
+    return 0
+
+
+def time_decompose(torch, np, workload, fs, args) -> int:
+    """Re-score the ISJL schedules of the headline workload (fsched_cost_decompose)."""
+    w = workload.WORKLOADS[args.workload]
+    a, p, o = workload.generate(w)
+    ta, tp, to = (torch.from_numpy(x).to("cuda:0") for x in (a, p, o))
+    kw = dict(B=w.B, alpha=w.alphas[0], M_kv=w.M_kv, cost_c=w.cost_c, cost_tau=w.cost_tau)
+    raw, st, _ = fs.simulate(ta, tp, to, policy="isjl", schedule=True, **kw)
+    torch.cuda.synchronize()
+    steps_per_call = int(fs.metrics_view(raw)["T"].sum())
+    for _ in range(args.warmup):
+        fs.cost_decompose(ta, tp, to, st, **kw)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        fs.cost_decompose(ta, tp, to, st, **kw)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / args.steps
+    print(json.dumps({"mode": "decompose", "workload": w.name, "ms_per_call": dt * 1e3,
+                      "instance_steps_per_s": steps_per_call / dt}))
+    return 0
+
+
+def time_opt(torch, np, workload, fs, args) -> int:
+    """Exact optima of the tiny adversarial workload (fsched_bruteforce_opt), one
+    (alpha, M_kv) setting per call over every instance."""
+    w = workload.WORKLOADS["tiny_opt_1048576x8"]
+    a, p, o = workload.generate(w)
+    ta, tp, to = (torch.from_numpy(x).to("cuda:0") for x in (a, p, o))
+    res = {}
+    for M in (w.M_kv, 0):
+        for al in w.alphas:
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(max(1, args.steps)):
+                fs.bruteforce_opt(ta, tp, to, B=w.B, alpha=al, M_kv=M)
+            torch.cuda.synchronize()
+            dt = (time.perf_counter() - t0) / max(1, args.steps)
+            res[f"M_kv={M},alpha={al}"] = {"s_per_call": dt, "solves_per_s": w.n_inst / dt}
+    print(json.dumps({"mode": "opt", "workload": w.name, "results": res}))
     return 0
 
 
