@@ -790,6 +790,133 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
       S.max_s = t;
     }
 
+    // Pure drain: LJF between batches, ISJL in DRAIN with nothing planned.  No
+    // job can be admitted before the machine is empty, so every remaining
+    // completion is an event with no decision attached.  The active jobs are
+    // sorted by completion and each span between consecutive completions is
+    // accounted in parallel: the jobs active in the span after position i are
+    // the positions > i, whose count, start sum and start range are suffix scans.
+    if ((POL == POL_LJF || (POL == POL_ISJL && mode == 1 && planned == 0)) && S.nact > 0) {
+      uint32_t* DK = W + a.off_drain;              // (end - t) << 11 | entry
+      int32_t* DG = (int32_t*)(DK + a.drain_nb);   // progress t - start of each entry
+      const int N = S.nact;
+      int NB = 64;
+      while (NB < N) NB <<= 1;
+      {
+        int base = 0;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const bool act = ws_end[k] != IDLE;
+          const uint64_t bm = ballot(act);
+          const int idx = base + mbcnt(bm);
+          if (act) {
+            DK[idx] = ((uint32_t)(ws_end[k] - t) << 11) | (uint32_t)idx;
+            DG[idx] = t - ws_start[k];
+            ws_end[k] = IDLE;
+            ws_start[k] = IDLE;
+          }
+          base += __builtin_popcountll(bm);
+        }
+        for (int i = N + lane; i < NB; i += WAVE) DK[i] = 0xFFFFFFFFu;
+        wave_lds_sync();
+        wave_bitonic_sort(DK, NB, lane);
+      }
+      // span [t, e_0): all N jobs
+      const int e0 = t + (int)(DK[0] >> 11);
+      int64_t lE = 0, lC = 0, lW = 0, lX = 0, lB = 0, lU = 0, lP = 0;
+      int lXm = 0, lAm = 0;
+      {
+        const int64_t D = (int64_t)(e0 - t), s = N;
+        const int64_t m0 = (int64_t)(t - S.min_s) + 1;
+        const int64_t sm = D * m0 + D * (D - 1) / 2;
+        if (lane == 0) {
+          lE = D * (S.sum_s - s * (int64_t)S.min_s);
+          lC = a.c * D + a.tau * s * sm;
+          lW = a.c * D + a.tau * sm;
+          const int ext = S.max_s - S.min_s;
+          lX = D * ext;
+          lB = D;
+          lU = ext > alpha ? D : 0;
+          lXm = ext;
+          lAm = N;
+          lP = s * (int64_t)e0 - S.sum_s;
+        }
+      }
+      // suffix sweep, last chunk first; lane L holds position c0 + 63 - L
+      int c_cnt = 0, c_g = 0, c_gmin = IDLE, c_gmax = -1;
+      int t_last = e0;
+      for (int c0 = ((N - 1) / WAVE) * WAVE; c0 >= 0; c0 -= WAVE) {
+        const int pos = c0 + (WAVE - 1) - lane;
+        const bool valid = pos < N;
+        const uint32_t key = valid ? DK[pos] : 0u;
+        const int e = t + (int)(key >> 11);
+        const int g = valid ? DG[key & 0x7FFu] : 0;
+        const int e_next = (pos + 1 < N) ? t + (int)(DK[pos + 1] >> 11) : e;
+        if (pos == N - 1) t_last = e;
+        const int icnt = wave_scan_incl(valid ? 1 : 0);
+        const int ig = wave_scan_incl(valid ? g : 0);
+        const int igmax = wave_scan_incl_max(valid ? g : (int)0x80000000);
+        const int igmin = wave_scan_incl_min(valid ? g : IDLE);
+        // exclusive (positions after this one inside the chunk) + carry
+        int pcnt = __shfl_up(icnt, 1), pg = __shfl_up(ig, 1);
+        int pgmax = __shfl_up(igmax, 1), pgmin = __shfl_up(igmin, 1);
+        if (lane == 0) {
+          pcnt = 0;
+          pg = 0;
+          pgmax = -1;
+          pgmin = IDLE;
+        }
+        const int cnt = c_cnt + pcnt;
+        const int gsum = c_g + pg;
+        const int gmax = max(c_gmax, pgmax), gmin = min(c_gmin, pgmin);
+        const int64_t D = (int64_t)(e_next - e);
+        if (valid && D > 0) {
+          const int64_t s = cnt;
+          const int min_s = t - gmax, max_s = t - gmin;
+          const int64_t sum_s = s * (int64_t)t - gsum;
+          const int64_t m0 = (int64_t)(e - min_s) + 1;
+          const int64_t sm = D * m0 + D * (D - 1) / 2;
+          lE += D * (sum_s - s * (int64_t)min_s);
+          lC += a.c * D + a.tau * s * sm;
+          lW += a.c * D + a.tau * sm;
+          const int ext = max_s - min_s;
+          lX += D * ext;
+          lB += D;
+          if (ext > alpha) lU += D;
+          lXm = max(lXm, ext);
+          lAm = max(lAm, cnt);
+          lP = max(lP, s * (int64_t)e_next - sum_s);
+        }
+        c_cnt += readlane(icnt, 63);
+        c_g += readlane(ig, 63);
+        c_gmax = max(c_gmax, readlane(igmax, 63));
+        c_gmin = min(c_gmin, readlane(igmin, 63));
+      }
+      t_last = wave_max(t_last);
+      acc_E += wave_sum64(lE);
+      acc_C += wave_sum64(lC);
+      acc_W += wave_sum64(lW);
+      acc_ext += wave_sum64(lX);
+      acc_busy += wave_sum64(lB);
+      acc_unfair += wave_sum64(lU);
+      acc_peak = max(acc_peak, wave_max64(lP));
+      acc_maxext = max(acc_maxext, wave_max(lXm));
+      acc_maxact = max(acc_maxact, wave_max(lAm));
+      S.ndone += N;
+      S.nact = 0;
+      S.res = 0;
+      S.sum_s = 0;
+      S.min_s = IDLE;
+      S.max_s = -1;
+      S.min_end = IDLE;
+      S.t = t_last;
+      if (++iter > iter_max) {
+        failed = true;
+        break;
+      }
+      continue;
+    }
+
     // (5) next event
     int tn = S.min_end;
     if (POL == POL_FCFS || !GEN) {

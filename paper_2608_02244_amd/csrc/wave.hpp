@@ -108,6 +108,44 @@ __device__ __forceinline__ int wave_scan_incl(int x) {
   return v;
 }
 
+// Inclusive prefix max over lanes 0..63 (identity INT_MIN).
+__device__ __forceinline__ int wave_scan_incl_max(int x) {
+  constexpr int ID = (int)0x80000000;
+  int v = x;
+  v = max(v, dpp<DPP_ROW_SHR1, 0xf, 0xf, false>(ID, x));
+  v = max(v, dpp<DPP_ROW_SHR2, 0xf, 0xf, false>(ID, x));
+  v = max(v, dpp<DPP_ROW_SHR3, 0xf, 0xf, false>(ID, x));
+  v = max(v, dpp<DPP_ROW_SHR4, 0xf, 0xe, false>(ID, v));
+  v = max(v, dpp<DPP_ROW_SHR8, 0xf, 0xc, false>(ID, v));
+  v = max(v, dpp<DPP_BCAST15, 0xa, 0xf, false>(ID, v));
+  v = max(v, dpp<DPP_BCAST31, 0xc, 0xf, false>(ID, v));
+  return v;
+}
+
+// Inclusive prefix min over lanes 0..63 (identity INT_MAX).
+__device__ __forceinline__ int wave_scan_incl_min(int x) {
+  constexpr int ID = 0x7FFFFFFF;
+  int v = x;
+  v = min(v, dpp<DPP_ROW_SHR1, 0xf, 0xf, false>(ID, x));
+  v = min(v, dpp<DPP_ROW_SHR2, 0xf, 0xf, false>(ID, x));
+  v = min(v, dpp<DPP_ROW_SHR3, 0xf, 0xf, false>(ID, x));
+  v = min(v, dpp<DPP_ROW_SHR4, 0xf, 0xe, false>(ID, v));
+  v = min(v, dpp<DPP_ROW_SHR8, 0xf, 0xc, false>(ID, v));
+  v = min(v, dpp<DPP_BCAST15, 0xa, 0xf, false>(ID, v));
+  v = min(v, dpp<DPP_BCAST31, 0xc, 0xf, false>(ID, v));
+  return v;
+}
+
+// 64-bit max through cross-lane shuffles (used outside the hot loop).
+__device__ __forceinline__ int64_t wave_max64(int64_t v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    int64_t o = __shfl_xor(v, off);
+    v = o > v ? o : v;
+  }
+  return uni64(v);
+}
+
 // 64-bit sum through cross-lane shuffles (used outside the hot loop).
 __device__ __forceinline__ int64_t wave_sum64(int64_t v) {
 #pragma unroll
