@@ -97,7 +97,7 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
   const bool isjl = p->policy == FSCHED_ISJL;
   const bool drains = isjl || p->policy == FSCHED_LJF;
   const int q_words = isjl ? NP / 2 : 0;
-  const int stage_words = isjl ? (Beff + 1) / 2 : 0;
+  const int stage_words = p->policy != FSCHED_FCFS ? (Beff + 1) / 2 : 0;
   const int drain_nb = next_pow2(Beff);
   const int drain_words = drains ? drain_nb + Beff : 0;  // sort keys + progress per entry
 

@@ -353,6 +353,80 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
     if (fi_out) fi_out[id] = t + len;
   };
 
+  // The first G queued ranks, in priority order, into STG[0..G).
+  auto gather_first = [&](int G) {
+    int gbase = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const int cnt = __builtin_popcount(pool.w[i]);
+      const int incl = wave_scan_incl(cnt);
+      int pos = gbase + incl - cnt;
+      uint32_t x = pool.w[i];
+      const int base = (i * WAVE + lane) << 5;
+      while (x && pos < G) {
+        const int b = __builtin_ctz(x);
+        x &= x - 1u;
+        STG[pos] = (uint16_t)(base + b);
+        pos++;
+      }
+      gbase += readlane(incl, 63);
+    }
+    wave_lds_sync();
+  };
+
+  // Admit at step t the longest prefix of STG[0..G) that fits the KV budget
+  // (strict order; a job that would run alone always fits), onto the first
+  // eligible idle workers in index order (ISJL Phase TWO also needs an empty
+  // plan queue).  Returns the number admitted.
+  auto admit_prefix = [&](int t, int G, bool need_empty_queue, int& adm, int64_t& adm_len,
+                          int& adm_minlen) -> int {
+    int na = G;
+    if (M != 0) {
+      int64_t run = S.res;
+      for (int c0 = 0; c0 < G; c0 += WAVE) {
+        const int j = c0 + lane;
+        const int len = j < G ? plen(W[STG[j]]) : 0;
+        const int pre = wave_scan_incl(len);
+        const bool fail = j < G && (j > 0 || S.nact > 0) && (run + pre > M);
+        const uint64_t fm = ballot(fail);
+        if (fm) {
+          na = c0 + __builtin_ctzll(fm);
+          break;
+        }
+        run += readlane(pre, 63);
+      }
+    }
+    if (na == 0) return 0;
+    int base = 0, lsum = 0, lmin = IDLE;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      if (base < na) {
+        const bool el = valid[k] && ws_end[k] == IDLE &&
+                        (!need_empty_queue || (ws_q[k] & 0xFFFFu) == QNONE);
+        const uint64_t bm = ballot(el);
+        const int idx = base + mbcnt(bm);
+        if (el && idx < na) {
+          const uint32_t wv = W[STG[idx]];
+          const int len = plen(wv);
+          ws_start[k] = t;
+          ws_end[k] = t + len;
+          emit(pid(wv), t, len);
+          lsum += len;
+          lmin = min(lmin, len);
+        }
+        base += __builtin_popcountll(bm);
+      }
+    }
+    const int tot = wave_sum(lsum);
+    adm_minlen = min(adm_minlen, wave_min(lmin));
+    pool.clear_upto(STG[na - 1], lane);  // the first na queued ranks
+    adm += na;
+    adm_len += tot;
+    S.res += tot;
+    S.nact += na;
+    return na;
+  };
+
   while (true) {
     const int t = S.t;
     // (1) retire the jobs whose last token was processed at t-1
@@ -469,33 +543,14 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
       head += done;
     } else if (POL == POL_LJF || POL == POL_SJF) {
       if (POL == POL_SJF || S.nact == 0) {
-        while (S.nact < Beff) {
-          int r = pool.first();
-          if (r < 0) break;
-          uint32_t wv = W[r];
-          int len = plen(wv);
-          if (M != 0 && S.nact > 0 && S.res + len > M) break;
-          pool.reset(r, lane);
-          int slot = -1;
-#pragma unroll
-          for (int k = 0; k < K; ++k) {
-            if (slot < 0) {
-              uint64_t bm = ballot(valid[k] && ws_end[k] == IDLE);
-              if (bm) slot = k * WAVE + __builtin_ctzll(bm);
-            }
+        const int freew = Beff - S.nact;
+        if (freew > 0) {
+          const int kp = pool.count();
+          const int G = min(freew, kp);
+          if (G > 0) {
+            gather_first(G);
+            admit_prefix(t, G, false, adm, adm_len, adm_minlen);
           }
-#pragma unroll
-          for (int k = 0; k < K; ++k)
-            if (k == (slot >> 6) && lane == (slot & 63)) {
-              ws_start[k] = t;
-              ws_end[k] = t + len;
-            }
-          if (lane == 0) emit(pid(wv), t, len);
-          adm++;
-          adm_len += len;
-          adm_minlen = min(adm_minlen, len);
-          S.res += len;
-          S.nact++;
         }
       }
     } else {  // ISJL
@@ -505,26 +560,7 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
         if (kp > 0) {
           mode = 0;
           int G = min(Beff, kp);
-          // gather the first G queued ranks (longest first) into STG
-          {
-            int gbase = 0;
-#pragma unroll
-            for (int i = 0; i < NW; ++i) {
-              int cnt = __builtin_popcount(pool.w[i]);
-              int incl = wave_scan_incl(cnt);
-              int pos = gbase + incl - cnt;
-              uint32_t x = pool.w[i];
-              int base = (i * WAVE + lane) << 5;
-              while (x && pos < G) {
-                int b = __builtin_ctz(x);
-                x &= x - 1u;
-                STG[pos] = (uint16_t)(base + b);
-                pos++;
-              }
-              gbase += readlane(incl, 63);
-            }
-            wave_lds_sync();
-          }
+          gather_first(G);  // longest first
           // Bp: largest prefix of the longest jobs that fits the KV budget
           int Bp = G;
           if (M != 0) {
@@ -746,39 +782,23 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
       // Phase TWO (FILL): idle workers with nothing planned take the longest
       // queued unplanned job while A_max(t) <= alpha; otherwise DRAIN.
       if (mode == 0) {
-        while (true) {
-          int wsel = -1;
+        int ie = 0;
 #pragma unroll
-          for (int k = 0; k < K; ++k) {
-            uint64_t bm = ballot(valid[k] && ws_end[k] == IDLE && (ws_q[k] & 0xFFFFu) == QNONE);
-            if (wsel < 0 && bm) wsel = k * WAVE + __builtin_ctzll(bm);
-          }
-          if (wsel < 0) break;
-          int r = pool.first();
-          if (r < 0) break;
-          if (amax > alpha) {
-            mode = 1;
-            break;
-          }
-          uint32_t wv = W[r];
-          int len = plen(wv);
-          if (M != 0 && S.nact > 0 && S.res + len > M) {
-            kv_block = true;
-            break;
-          }
-          pool.reset(r, lane);
-#pragma unroll
-          for (int k = 0; k < K; ++k)
-            if (k == (wsel >> 6) && lane == (wsel & 63)) {
-              ws_start[k] = t;
-              ws_end[k] = t + len;
+        for (int k = 0; k < K; ++k)
+          ie += (valid[k] && ws_end[k] == IDLE && (ws_q[k] & 0xFFFFu) == QNONE) ? 1 : 0;
+        const int nie = wave_sum(ie);
+        if (nie > 0) {
+          const int kp = pool.count();
+          if (kp > 0) {
+            if (amax > alpha) {
+              mode = 1;
+            } else {
+              const int G = min(nie, kp);
+              gather_first(G);
+              const int na = admit_prefix(t, G, true, adm, adm_len, adm_minlen);
+              if (na < G) kv_block = true;
             }
-          if (lane == 0) emit(pid(wv), t, len);
-          adm++;
-          adm_len += len;
-          adm_minlen = min(adm_minlen, len);
-          S.res += len;
-          S.nact++;
+          }
         }
       }
     }
