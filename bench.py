@@ -25,6 +25,31 @@ METRIC = "instance-steps/sec (ISJL, 1 MI355X) + fraction of gfx950 VALU/LDS/HBM 
 UNIT = "instance-steps/s"
 # gfx950: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = int32 VALU lane operations per second
 PEAK_ALU = 256 * 64 * 2.4e9
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "simulate_isjl_pareto_65536x2000_hbm.md")
+KERNEL_SOURCES = ["sim_kernel.hpp", "sim_common.hpp", "wave.hpp", "sim_isjl.hip", "abi.cpp"]
+
+
+def kernel_sources_sha256() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_02244_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per launch from the committed counter summary, or None once the
+    kernel sources differ from the ones the counters were taken with."""
+    try:
+        text = open(TRAFFIC_SUMMARY).read()
+    except OSError:
+        return None
+    vals = dict(line.split(": ", 1) for line in text.splitlines() if ": " in line and
+                line.split(": ", 1)[0] in ("traffic_bytes_per_launch", "kernel_sources_sha256"))
+    if vals.get("kernel_sources_sha256", "").strip() != kernel_sources_sha256():
+        return None
+    return int(vals["traffic_bytes_per_launch"])
 
 
 def algorithmic_ops(n_inst: int, n: int, B: int, policy: str, sorted_arrivals: bool) -> float:
@@ -117,7 +142,7 @@ def main() -> int:
     achieved = ops / avg_launch_s
     roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_ALU / 1e12,
                 "unit": "Tops/s (int32 lane operations)", "frac": achieved / PEAK_ALU,
-                "traffic": None, "kernel": f"simulate_kernel<ISJL> ({w.n_inst} waves)",
+                "traffic": measured_traffic(), "kernel": f"simulate_kernel<ISJL> ({w.n_inst} waves)",
                 "avg_launch_ms": avg_launch_s * 1e3, "ops_per_launch": ops}
 
     out = {"metric": METRIC, "value": value, "unit": UNIT, "n_gpus": 1, "steps": args.steps,
