@@ -497,6 +497,7 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
     int adm = 0, adm_minlen = IDLE;
     int64_t adm_len = 0;
     bool kv_block = false;
+    int free_empty = 0;  // ISJL: idle workers with nothing planned, after this step's admissions
 
     // (4) admissions
     if (POL == POL_FCFS) {
@@ -787,6 +788,7 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
         for (int k = 0; k < K; ++k)
           ie += (valid[k] && ws_end[k] == IDLE && (ws_q[k] & 0xFFFFu) == QNONE) ? 1 : 0;
         const int nie = wave_sum(ie);
+        free_empty = nie;
         if (nie > 0) {
           const int kp = pool.count();
           if (kp > 0) {
@@ -796,6 +798,7 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
               const int G = min(nie, kp);
               gather_first(G);
               const int na = admit_prefix(t, G, true, adm, adm_len, adm_minlen);
+              free_empty = nie - na;
               if (na < G) kv_block = true;
             }
           }
@@ -937,15 +940,25 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
       continue;
     }
 
-    // (5) next event
+    // (5) next event.  A release is an event only if the job could be admitted
+    // before anything else happens: ISJL with an idle worker that has nothing
+    // planned in Phase TWO, or an empty machine with no plan; LJF at an empty
+    // machine; FCFS / SJF with a free slot.  Otherwise it is folded into the
+    // next event (the queue is only read there).
     int tn = S.min_end;
-    if (POL == POL_FCFS || !GEN) {
-      if (relk < n) {
-        if ((relk >> 6) != chunk) load_chunk(relk >> 6);
-        tn = min(tn, readlane(rel_t, relk & 63));
+    bool rel_matters;
+    if (POL == POL_ISJL) rel_matters = (mode == 0 && free_empty > 0) || (S.nact == 0 && planned == 0);
+    else if (POL == POL_LJF) rel_matters = S.nact == 0;
+    else rel_matters = S.nact < Beff;
+    if (rel_matters) {
+      if (POL == POL_FCFS || !GEN) {
+        if (relk < n) {
+          if ((relk >> 6) != chunk) load_chunk(relk >> 6);
+          tn = min(tn, readlane(rel_t, relk & 63));
+        }
+      } else {
+        tn = min(tn, next_rel);
       }
-    } else {
-      tn = min(tn, next_rel);
     }
     if (POL == POL_ISJL) {
       if (planned > 0 && t_w1 > t) {
