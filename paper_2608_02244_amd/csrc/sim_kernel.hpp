@@ -612,57 +612,63 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
             // each goes to the first spare worker with room, else to the long
             // worker of largest index with room; a job that fits nowhere stays.
             int cur = rlast;
+            const bool has_spare = Bp > m;
             while (true) {
-              int rm = -1;
-#pragma unroll
-              for (int k = 0; k < K; ++k) rm = max(rm, cap[k] - load[k]);
-              int remmax = wave_max(rm);
-              if (remmax <= 0) break;
-              int r = pool.first_from(cur + 1, lane);
+              const int r = pool.first_from(cur + 1, lane);
               if (r < 0) break;
-              int len = plen(W[r]);
-              if (len > remmax) {
-                // first rank >= r with len <= remmax (lengths are non-increasing)
-                int span = n - r;
-                int s = (span + WAVE - 1) / WAVE;
-                int p = r + lane * s;
-                bool ok = p < n && plen(W[p]) <= remmax;
-                uint64_t fm = ballot(ok);
-                int lo, hi;
-                if (fm) {
-                  int L1 = __builtin_ctzll(fm);
-                  hi = r + L1 * s;
-                  lo = L1 > 0 ? r + (L1 - 1) * s + 1 : r;
-                } else {
-                  // after the last probe inside [r, n)
-                  lo = r + ((span - 1) / s) * s + 1;
-                  hi = n;
-                }
-                int q = lo + lane;
-                bool ok2 = q < hi && plen(W[q]) <= remmax;
-                uint64_t fm2 = ballot(ok2);
-                int b = fm2 ? lo + __builtin_ctzll(fm2) : hi;
-                if (b >= n) break;
-                r = pool.first_from(b, lane);
-                if (r < 0) break;
-                len = plen(W[r]);
-              }
+              const int len = plen(W[r]);
               int wsel = -1;
+              if (has_spare) {  // spare workers, ascending
 #pragma unroll
-              for (int k = 0; k < K; ++k) {
-                int w = k * WAVE + lane;
-                uint64_t ms = ballot(w >= m && w < Bp && cap[k] - load[k] >= len);
-                if (wsel < 0 && ms) wsel = k * WAVE + __builtin_ctzll(ms);
+                for (int k = 0; k < K; ++k) {
+                  const int w = k * WAVE + lane;
+                  const uint64_t ms = ballot(w >= m && w < Bp && cap[k] - load[k] >= len);
+                  if (ms) {
+                    wsel = k * WAVE + __builtin_ctzll(ms);
+                    break;
+                  }
+                }
               }
-              if (wsel < 0) {
+              if (wsel < 0) {  // long workers, largest index first
 #pragma unroll
                 for (int k = K - 1; k >= 0; --k) {
-                  int w = k * WAVE + lane;
-                  uint64_t ml = ballot(w >= 1 && w < m && cap[k] - load[k] >= len);
-                  if (wsel < 0 && ml) wsel = k * WAVE + 63 - __builtin_clzll(ml);
+                  const int w = k * WAVE + lane;
+                  const uint64_t ml = ballot(w >= 1 && w < m && cap[k] - load[k] >= len);
+                  if (ml) {
+                    wsel = k * WAVE + 63 - __builtin_clzll(ml);
+                    break;
+                  }
                 }
               }
-              if (wsel < 0) break;  // unreachable: len <= remmax
+              if (wsel < 0) {
+                // r fits nowhere: skip to the first rank whose length fits the
+                // largest room left (lengths are non-increasing in rank)
+                int rm = -1;
+#pragma unroll
+                for (int k = 0; k < K; ++k) rm = max(rm, cap[k] - load[k]);
+                const int remmax = wave_max(rm);
+                if (remmax <= 0) break;
+                const int span = n - r;
+                const int sstep = (span + WAVE - 1) / WAVE;
+                const int p = r + lane * sstep;
+                const uint64_t fm = ballot(p < n && plen(W[p]) <= remmax);
+                int lo, hi;
+                if (fm) {
+                  const int L1 = __builtin_ctzll(fm);
+                  hi = r + L1 * sstep;
+                  lo = L1 > 0 ? r + (L1 - 1) * sstep + 1 : r;
+                } else {
+                  // after the last probe inside [r, n)
+                  lo = r + ((span - 1) / sstep) * sstep + 1;
+                  hi = n;
+                }
+                const int q = lo + lane;
+                const uint64_t fm2 = ballot(q < hi && plen(W[q]) <= remmax);
+                const int b = fm2 ? lo + __builtin_ctzll(fm2) : hi;
+                if (b >= n) break;
+                cur = b - 1;
+                continue;
+              }
               // append r to worker wsel's queue
               int qt = (int)QNONE;
 #pragma unroll
@@ -813,13 +819,20 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
       S.max_s = t;
     }
 
-    // Pure drain: LJF between batches, ISJL in DRAIN with nothing planned.  No
-    // job can be admitted before the machine is empty, so every remaining
-    // completion is an event with no decision attached.  The active jobs are
-    // sorted by completion and each span between consecutive completions is
-    // accounted in parallel: the jobs active in the span after position i are
-    // the positions > i, whose count, start sum and start range are suffix scans.
-    if ((POL == POL_LJF || (POL == POL_ISJL && mode == 1 && planned == 0)) && S.nact > 0) {
+    // Drain sweep.  LJF between batches and ISJL in DRAIN admit nothing through
+    // Phase TWO, and a planned ISJL job can start only at a step where
+    // A_max(t) <= alpha, which (A_max grows between completions) can first hold
+    // right after a completion, or when the machine is empty.  Every completion
+    // before that carries no decision: the active jobs are sorted by
+    // completion and each span between consecutive completions is accounted in
+    // parallel, the jobs active after position i being the positions > i (their
+    // count, progress sum and progress range are suffix scans).  The sweep
+    // stops at the first completion after which a planned job could start; the
+    // jobs still active there stay in their slots.
+    const bool w0_timer = POL == POL_ISJL && planned > 0 && t_w1 > t &&
+                          readlane(ws_end[0], 0) == IDLE &&
+                          ((uint32_t)readlane((int)ws_q[0], 0) & 0xFFFFu) != QNONE;
+    if ((POL == POL_LJF || (POL == POL_ISJL && mode == 1 && !w0_timer)) && S.nact > 0) {
       uint32_t* DK = W + a.off_drain;              // (end - t) << 11 | entry
       int32_t* DG = (int32_t*)(DK + a.drain_nb);   // progress t - start of each entry
       const int N = S.nact;
@@ -835,8 +848,6 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
           if (act) {
             DK[idx] = ((uint32_t)(ws_end[k] - t) << 11) | (uint32_t)idx;
             DG[idx] = t - ws_start[k];
-            ws_end[k] = IDLE;
-            ws_start[k] = IDLE;
           }
           base += __builtin_popcountll(bm);
         }
@@ -844,78 +855,102 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
         wave_lds_sync();
         wave_bitonic_sort(DK, NB, lane);
       }
-      // span [t, e_0): all N jobs
-      const int e0 = t + (int)(DK[0] >> 11);
+      // One backward pass over the sorted positions (lane L holds position
+      // c0 + 63 - L).  stop < 0: find the stop position (the lowest position
+      // ending a tie group after which the machine is empty or A_max <= alpha);
+      // otherwise accumulate the spans of the positions below `stop` and return
+      // the suffix state just after `stop`.
       int64_t lE = 0, lC = 0, lW = 0, lX = 0, lB = 0, lU = 0, lP = 0;
       int lXm = 0, lAm = 0;
+      int st_cnt = 0, st_g = 0, st_gmax = -1, st_gmin = IDLE;  // state after `stop`
+      auto pass = [&](int stop) -> int {
+        int c_cnt = 0, c_g = 0, c_gmin = IDLE, c_gmax = -1;
+        int found = N - 1;
+        for (int c0 = ((N - 1) / WAVE) * WAVE; c0 >= 0; c0 -= WAVE) {
+          const int pos = c0 + (WAVE - 1) - lane;
+          const bool valid = pos < N;
+          const uint32_t key = valid ? DK[pos] : 0u;
+          const int e = t + (int)(key >> 11);
+          const int g = valid ? DG[key & 0x7FFu] : 0;
+          const int e_next = (pos + 1 < N) ? t + (int)(DK[pos + 1] >> 11) : e;
+          const int icnt = wave_scan_incl(valid ? 1 : 0);
+          const int ig = wave_scan_incl(valid ? g : 0);
+          const int igmax = wave_scan_incl_max(valid ? g : (int)0x80000000);
+          const int igmin = wave_scan_incl_min(valid ? g : IDLE);
+          int pcnt = __shfl_up(icnt, 1), pg = __shfl_up(ig, 1);
+          int pgmax = __shfl_up(igmax, 1), pgmin = __shfl_up(igmin, 1);
+          if (lane == 0) {
+            pcnt = 0;
+            pg = 0;
+            pgmax = -1;
+            pgmin = IDLE;
+          }
+          const int cnt = c_cnt + pcnt;
+          const int gsum = c_g + pg;
+          const int gmax = max(c_gmax, pgmax), gmin = min(c_gmin, pgmin);
+          if (stop < 0) {
+            // A_max right after the completions at e: e - (t - gmax)
+            const bool group_end = valid && (pos + 1 >= N || e_next > e);
+            const bool ok = group_end && (cnt == 0 || e - t + gmax <= alpha);
+            const uint64_t mk = ballot(ok);
+            if (mk) found = min(found, c0 + (WAVE - 1) - (63 - __builtin_clzll(mk)));
+          } else {
+            const int64_t D = (int64_t)(e_next - e);
+            if (valid && pos < stop && D > 0) {
+              const int64_t s = cnt;
+              const int min_s = t - gmax, max_s = t - gmin;
+              const int64_t sum_s = s * (int64_t)t - gsum;
+              const int64_t m0 = (int64_t)(e - min_s) + 1;
+              const int64_t sm = D * m0 + D * (D - 1) / 2;
+              lE += D * (sum_s - s * (int64_t)min_s);
+              lC += a.c * D + a.tau * s * sm;
+              lW += a.c * D + a.tau * sm;
+              const int ext = max_s - min_s;
+              lX += D * ext;
+              lB += D;
+              if (ext > alpha) lU += D;
+              lXm = max(lXm, ext);
+              lAm = max(lAm, cnt);
+              lP = max(lP, s * (int64_t)e_next - sum_s);
+            }
+            const uint64_t hs = ballot(valid && pos == stop);
+            if (hs) {
+              const int L = __builtin_ctzll(hs);
+              st_cnt = readlane(cnt, L);
+              st_g = readlane(gsum, L);
+              st_gmax = readlane(gmax, L);
+              st_gmin = readlane(gmin, L);
+            }
+          }
+          c_cnt += readlane(icnt, 63);
+          c_g += readlane(ig, 63);
+          c_gmax = max(c_gmax, readlane(igmax, 63));
+          c_gmin = min(c_gmin, readlane(igmin, 63));
+        }
+        return found;
+      };
+      const int stop = (POL == POL_ISJL && planned > 0) ? pass(-1) : N - 1;
+      pass(stop);
+      const int tau_end = t + (int)(DK[stop] >> 11);
+      // span [t, e_0): every job still active
       {
+        const int e0 = t + (int)(DK[0] >> 11);
         const int64_t D = (int64_t)(e0 - t), s = N;
         const int64_t m0 = (int64_t)(t - S.min_s) + 1;
         const int64_t sm = D * m0 + D * (D - 1) / 2;
         if (lane == 0) {
-          lE = D * (S.sum_s - s * (int64_t)S.min_s);
-          lC = a.c * D + a.tau * s * sm;
-          lW = a.c * D + a.tau * sm;
-          const int ext = S.max_s - S.min_s;
-          lX = D * ext;
-          lB = D;
-          lU = ext > alpha ? D : 0;
-          lXm = ext;
-          lAm = N;
-          lP = s * (int64_t)e0 - S.sum_s;
-        }
-      }
-      // suffix sweep, last chunk first; lane L holds position c0 + 63 - L
-      int c_cnt = 0, c_g = 0, c_gmin = IDLE, c_gmax = -1;
-      int t_last = e0;
-      for (int c0 = ((N - 1) / WAVE) * WAVE; c0 >= 0; c0 -= WAVE) {
-        const int pos = c0 + (WAVE - 1) - lane;
-        const bool valid = pos < N;
-        const uint32_t key = valid ? DK[pos] : 0u;
-        const int e = t + (int)(key >> 11);
-        const int g = valid ? DG[key & 0x7FFu] : 0;
-        const int e_next = (pos + 1 < N) ? t + (int)(DK[pos + 1] >> 11) : e;
-        if (pos == N - 1) t_last = e;
-        const int icnt = wave_scan_incl(valid ? 1 : 0);
-        const int ig = wave_scan_incl(valid ? g : 0);
-        const int igmax = wave_scan_incl_max(valid ? g : (int)0x80000000);
-        const int igmin = wave_scan_incl_min(valid ? g : IDLE);
-        // exclusive (positions after this one inside the chunk) + carry
-        int pcnt = __shfl_up(icnt, 1), pg = __shfl_up(ig, 1);
-        int pgmax = __shfl_up(igmax, 1), pgmin = __shfl_up(igmin, 1);
-        if (lane == 0) {
-          pcnt = 0;
-          pg = 0;
-          pgmax = -1;
-          pgmin = IDLE;
-        }
-        const int cnt = c_cnt + pcnt;
-        const int gsum = c_g + pg;
-        const int gmax = max(c_gmax, pgmax), gmin = min(c_gmin, pgmin);
-        const int64_t D = (int64_t)(e_next - e);
-        if (valid && D > 0) {
-          const int64_t s = cnt;
-          const int min_s = t - gmax, max_s = t - gmin;
-          const int64_t sum_s = s * (int64_t)t - gsum;
-          const int64_t m0 = (int64_t)(e - min_s) + 1;
-          const int64_t sm = D * m0 + D * (D - 1) / 2;
-          lE += D * (sum_s - s * (int64_t)min_s);
+          lE += D * (S.sum_s - s * (int64_t)S.min_s);
           lC += a.c * D + a.tau * s * sm;
           lW += a.c * D + a.tau * sm;
-          const int ext = max_s - min_s;
+          const int ext = S.max_s - S.min_s;
           lX += D * ext;
           lB += D;
           if (ext > alpha) lU += D;
           lXm = max(lXm, ext);
-          lAm = max(lAm, cnt);
-          lP = max(lP, s * (int64_t)e_next - sum_s);
+          lAm = max(lAm, N);
+          lP = max(lP, s * (int64_t)e0 - S.sum_s);
         }
-        c_cnt += readlane(icnt, 63);
-        c_g += readlane(ig, 63);
-        c_gmax = max(c_gmax, readlane(igmax, 63));
-        c_gmin = min(c_gmin, readlane(igmin, 63));
       }
-      t_last = wave_max(t_last);
       acc_E += wave_sum64(lE);
       acc_C += wave_sum64(lC);
       acc_W += wave_sum64(lW);
@@ -925,14 +960,33 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
       acc_peak = max(acc_peak, wave_max64(lP));
       acc_maxext = max(acc_maxext, wave_max(lXm));
       acc_maxact = max(acc_maxact, wave_max(lAm));
-      S.ndone += N;
-      S.nact = 0;
-      S.res = 0;
-      S.sum_s = 0;
-      S.min_s = IDLE;
-      S.max_s = -1;
-      S.min_end = IDLE;
-      S.t = t_last;
+      // retire every job that completed by tau_end
+      int rc = 0, rl = 0, me = IDLE;
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        if (ws_end[k] <= tau_end) {
+          rc++;
+          rl += ws_end[k] - ws_start[k];
+          ws_end[k] = IDLE;
+          ws_start[k] = IDLE;
+        }
+        me = min(me, ws_end[k]);
+      }
+      const int nret = wave_sum(rc);
+      S.ndone += nret;
+      S.res -= wave_sum(rl);
+      S.nact = N - nret;
+      S.min_end = wave_min(me);
+      if (S.nact > 0) {
+        S.sum_s = (int64_t)st_cnt * t - st_g;
+        S.min_s = t - st_gmax;
+        S.max_s = t - st_gmin;
+      } else {
+        S.sum_s = 0;
+        S.min_s = IDLE;
+        S.max_s = -1;
+      }
+      S.t = tau_end;
       if (++iter > iter_max) {
         failed = true;
         break;
