@@ -95,11 +95,8 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
   const int NW = n <= 2048 ? 1 : 2;
   const int NP = next_pow2(n);
   const bool isjl = p->policy == FSCHED_ISJL;
-  const bool drains = isjl || p->policy == FSCHED_LJF;
   const int q_words = isjl ? NP / 2 : 0;
   const int stage_words = p->policy != FSCHED_FCFS ? (Beff + 1) / 2 : 0;
-  const int drain_nb = next_pow2(Beff);
-  const int drain_words = drains ? drain_nb + Beff : 0;  // sort keys + progress per entry
 
   fs::SimArgs a;
   std::memset(&a, 0, sizeof(a));
@@ -125,10 +122,7 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
     b.off_arr = NP;
     b.off_q = NP + (general ? NP : 0);
     b.off_stage = b.off_q + q_words;
-    b.off_drain = b.off_q;  // the plan queues are empty whenever the drain sweep runs
-    b.drain_nb = drain_nb;
     b.wave_words = b.off_stage + stage_words;
-    if (b.off_drain + drain_words > b.wave_words) b.wave_words = b.off_drain + drain_words;
     b.wave_words = (b.wave_words + 3) & ~3;
     size_t per_wave = (size_t)b.wave_words * 4;
     int wpb = 4;

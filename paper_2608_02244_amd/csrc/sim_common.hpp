@@ -30,8 +30,6 @@ struct SimArgs {
   int32_t off_arr;    // word offset of arrival-by-rank (general kernel)
   int32_t off_q;      // word offset of the plan-queue links (ISJL)
   int32_t off_stage;  // word offset of the gather buffer (ISJL)
-  int32_t off_drain;  // word offset of the drain-sweep buffers (LJF / ISJL)
-  int32_t drain_nb;   // sort length of the drain sweep (power of two >= Beff)
   int32_t pad;
   const int32_t* arrival;
   const int32_t* prompt;

@@ -25,7 +25,8 @@
 //   LDS   W[r]     jobs in the policy's priority order, packed (len << 12 | id)
 //         ARR[r]   arrival of rank r (general variant only)
 //         QN[r]    next job in the same ISJL plan queue (uint16, ISJL)
-//         STG[j]   gather buffer for Phase ONE (uint16, ISJL)
+//         STG[j]   gather buffer of the first queued ranks (uint16, not FCFS)
+//   The drain sweep sorts the active slots in registers and needs no LDS.
 //   VGPR  K worker slots per lane: worker w lives in slot w/64 of lane w%64
 //         (start, end, ISJL plan-queue head|tail); a bitmap of queued jobs over
 //         ranks (bit r%32 of word r/2048 in lane (r/32)%64).
@@ -60,6 +61,74 @@ __device__ inline void wave_bitonic_sort(uint32_t* W, int NP, int lane) {
         }
       }
       wave_lds_sync();
+    }
+  }
+}
+
+// Compare-exchange of positions p and p ^ D (D < 64: lanes of one register)
+// in a bitonic stage of block `size`; position p = k * 64 + lane.  The payload
+// follows its key; equal keys keep their own payloads, which is a valid
+// outcome of the exchange.
+template <int D, int K>
+__device__ __forceinline__ void reg_cx_lanes(uint32_t (&key)[K], int (&val)[K], int size,
+                                             int lane) {
+  const bool lower = (lane & D) == 0;
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const uint32_t pk = (uint32_t)shfl_xor_c<D>((int)key[k]);
+    const int pv = shfl_xor_c<D>(val[k]);
+    const bool asc = ((k * WAVE + lane) & size) == 0;
+    const uint32_t nk = (lower == asc) ? min(key[k], pk) : max(key[k], pk);
+    val[k] = nk == key[k] ? val[k] : pv;
+    key[k] = nk;
+  }
+}
+
+// Compare-exchange of registers k and k ^ DK (distance DK * 64 positions).
+template <int DK, int K>
+__device__ __forceinline__ void reg_cx_regs(uint32_t (&key)[K], int (&val)[K], int size) {
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    if ((k & DK) == 0) {
+      const int h = k | DK;
+      const bool asc = ((k * WAVE) & size) == 0;
+      const uint32_t x = key[k], y = key[h];
+      const int vx = val[k], vy = val[h];
+      const bool sw = (x > y) == asc;
+      key[k] = sw ? y : x;
+      key[h] = sw ? x : y;
+      val[k] = sw ? vy : vx;
+      val[h] = sw ? vx : vy;
+    }
+  }
+}
+
+// Bitonic sort, ascending, of the K * 64 keys held in registers (position
+// k * 64 + lane), each carrying one payload word.  No LDS is used.
+template <int K>
+__device__ inline void reg_bitonic_sort(uint32_t (&key)[K], int (&val)[K], int lane) {
+  for (int size = 2; size <= K * WAVE; size <<= 1) {
+    for (int d = size >> 1; d > 0; d >>= 1) {
+      switch (d) {
+        case 1: reg_cx_lanes<1>(key, val, size, lane); break;
+        case 2: reg_cx_lanes<2>(key, val, size, lane); break;
+        case 4: reg_cx_lanes<4>(key, val, size, lane); break;
+        case 8: reg_cx_lanes<8>(key, val, size, lane); break;
+        case 16: reg_cx_lanes<16>(key, val, size, lane); break;
+        case 32: reg_cx_lanes<32>(key, val, size, lane); break;
+        case 64:
+          if constexpr (K > 1) reg_cx_regs<1>(key, val, size);
+          break;
+        case 128:
+          if constexpr (K > 2) reg_cx_regs<2>(key, val, size);
+          break;
+        case 256:
+          if constexpr (K > 4) reg_cx_regs<4>(key, val, size);
+          break;
+        default:
+          if constexpr (K > 8) reg_cx_regs<8>(key, val, size);
+          break;
+      }
     }
   }
 }
@@ -155,7 +224,7 @@ struct SimState {
 };
 
 template <int POL, int K, int NW, bool GEN>
-__global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 : 1))) void simulate_kernel(SimArgs a) {
   extern __shared__ uint32_t lds_raw[];
   const int wib = threadIdx.x >> 6;
   const int64_t inst = (int64_t)blockIdx.x * (blockDim.x >> 6) + wib;
@@ -824,57 +893,60 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
     // A_max(t) <= alpha, which (A_max grows between completions) can first hold
     // right after a completion, or when the machine is empty.  Every completion
     // before that carries no decision: the active jobs are sorted by
-    // completion and each span between consecutive completions is accounted in
-    // parallel, the jobs active after position i being the positions > i (their
-    // count, progress sum and progress range are suffix scans).  The sweep
-    // stops at the first completion after which a planned job could start; the
-    // jobs still active there stay in their slots.
+    // completion (in registers) and each span between consecutive completions
+    // is accounted in parallel, the jobs active after position i being the
+    // positions > i (their count, progress sum and progress range are suffix
+    // scans).  The sweep stops at the first completion after which a planned
+    // job could start; the jobs still active there stay in their slots.
     const bool w0_timer = POL == POL_ISJL && planned > 0 && t_w1 > t &&
                           readlane(ws_end[0], 0) == IDLE &&
                           ((uint32_t)readlane((int)ws_q[0], 0) & 0xFFFFu) != QNONE;
     if ((POL == POL_LJF || (POL == POL_ISJL && mode == 1 && !w0_timer)) && S.nact > 0) {
-      uint32_t* DK = W + a.off_drain;              // (end - t) << 11 | entry
-      int32_t* DG = (int32_t*)(DK + a.drain_nb);   // progress t - start of each entry
       const int N = S.nact;
-      int NB = 64;
-      while (NB < N) NB <<= 1;
-      {
-        int base = 0;
+      uint32_t dk[K];  // end - t of each active slot (inactive: all ones), sorted
+      int dg[K];       // progress t - start, carried with its key
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-          const bool act = ws_end[k] != IDLE;
-          const uint64_t bm = ballot(act);
-          const int idx = base + mbcnt(bm);
-          if (act) {
-            DK[idx] = ((uint32_t)(ws_end[k] - t) << 11) | (uint32_t)idx;
-            DG[idx] = t - ws_start[k];
-          }
-          base += __builtin_popcountll(bm);
-        }
-        for (int i = N + lane; i < NB; i += WAVE) DK[i] = 0xFFFFFFFFu;
-        wave_lds_sync();
-        wave_bitonic_sort(DK, NB, lane);
+      for (int k = 0; k < K; ++k) {
+        const bool act = ws_end[k] != IDLE;
+        dk[k] = act ? (uint32_t)(ws_end[k] - t) : 0xFFFFFFFFu;
+        dg[k] = act ? t - ws_start[k] : 0;
       }
-      // One backward pass over the sorted positions (lane L holds position
-      // c0 + 63 - L).  stop < 0: find the stop position (the lowest position
-      // ending a tie group after which the machine is empty or A_max <= alpha);
-      // otherwise accumulate the spans of the positions below `stop` and return
-      // the suffix state just after `stop`.
+      reg_bitonic_sort<K>(dk, dg, lane);
+      // One backward pass over the sorted positions, a register at a time
+      // (reversed so that lane L holds position k * 64 + 63 - L).  stop < 0:
+      // find the stop position (the lowest position ending a tie group after
+      // which the machine is empty or A_max <= alpha); otherwise accumulate
+      // the spans of the positions below `stop` and return the suffix state
+      // just after `stop`.
       int64_t lE = 0, lC = 0, lW = 0, lX = 0, lB = 0, lU = 0, lP = 0;
       int lXm = 0, lAm = 0;
-      int st_cnt = 0, st_g = 0, st_gmax = -1, st_gmin = IDLE;  // state after `stop`
+      int st_cnt = 0, st_g = 0, st_gmax = -1, st_gmin = IDLE, st_e = t;  // state after `stop`
       auto pass = [&](int stop) -> int {
         int c_cnt = 0, c_g = 0, c_gmin = IDLE, c_gmax = -1;
         int found = N - 1;
-        for (int c0 = ((N - 1) / WAVE) * WAVE; c0 >= 0; c0 -= WAVE) {
-          const int pos = c0 + (WAVE - 1) - lane;
+        for (int k = (N - 1) / WAVE; k >= 0; --k) {
+          // register k of the sorted keys (a select chain keeps the arrays in
+          // registers with a loop that is not unrolled)
+          int kc = 0, gc = 0, kn0 = 0;
+#pragma unroll
+          for (int q = 0; q < K; ++q) {
+            if (q == k) {
+              kc = (int)dk[q];
+              gc = dg[q];
+            }
+            if (q == k + 1) kn0 = (int)dk[q];
+          }
+          const int pos = k * WAVE + (WAVE - 1) - lane;
           const bool valid = pos < N;
-          const uint32_t key = valid ? DK[pos] : 0u;
-          const int e = t + (int)(key >> 11);
-          const int g = valid ? DG[key & 0x7FFu] : 0;
-          const int e_next = (pos + 1 < N) ? t + (int)(DK[pos + 1] >> 11) : e;
+          const int kr = __shfl(kc, (WAVE - 1) - lane);
+          const int gr = __shfl(gc, (WAVE - 1) - lane);
+          const int e = t + (valid ? kr : 0);
+          const int g = valid ? gr : 0;
+          int kn = __shfl_up(kr, 1);
+          if (lane == 0) kn = readlane(kn0, 0);
+          const int e_next = (pos + 1 < N) ? t + kn : e;
           const int icnt = wave_scan_incl(valid ? 1 : 0);
-          const int ig = wave_scan_incl(valid ? g : 0);
+          const int ig = wave_scan_incl(g);
           const int igmax = wave_scan_incl_max(valid ? g : (int)0x80000000);
           const int igmin = wave_scan_incl_min(valid ? g : IDLE);
           int pcnt = __shfl_up(icnt, 1), pg = __shfl_up(ig, 1);
@@ -893,7 +965,7 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
             const bool group_end = valid && (pos + 1 >= N || e_next > e);
             const bool ok = group_end && (cnt == 0 || e - t + gmax <= alpha);
             const uint64_t mk = ballot(ok);
-            if (mk) found = min(found, c0 + (WAVE - 1) - (63 - __builtin_clzll(mk)));
+            if (mk) found = min(found, k * WAVE + __builtin_clzll(mk));
           } else {
             const int64_t D = (int64_t)(e_next - e);
             if (valid && pos < stop && D > 0) {
@@ -920,6 +992,7 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
               st_g = readlane(gsum, L);
               st_gmax = readlane(gmax, L);
               st_gmin = readlane(gmin, L);
+              st_e = readlane(e, L);
             }
           }
           c_cnt += readlane(icnt, 63);
@@ -931,10 +1004,10 @@ __global__ __launch_bounds__(256) void simulate_kernel(SimArgs a) {
       };
       const int stop = (POL == POL_ISJL && planned > 0) ? pass(-1) : N - 1;
       pass(stop);
-      const int tau_end = t + (int)(DK[stop] >> 11);
+      const int tau_end = st_e;
       // span [t, e_0): every job still active
       {
-        const int e0 = t + (int)(DK[0] >> 11);
+        const int e0 = t + readlane((int)dk[0], 0);
         const int64_t D = (int64_t)(e0 - t), s = N;
         const int64_t m0 = (int64_t)(t - S.min_s) + 1;
         const int64_t sm = D * m0 + D * (D - 1) / 2;

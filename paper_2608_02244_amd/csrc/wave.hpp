@@ -136,6 +136,19 @@ __device__ __forceinline__ int wave_scan_incl_min(int x) {
   return v;
 }
 
+// Value of lane (lane ^ D), D a power of two below 64: DPP for 1, 2 (quad
+// permutes) and 8 (rotate a row of 16 by 8), swizzle in bit mode for 4 and 16
+// (xor mask within 32 lanes), a permute through the LDS crossbar for 32.
+template <int D>
+__device__ __forceinline__ int shfl_xor_c(int v) {
+  static_assert(D > 0 && D < WAVE && (D & (D - 1)) == 0, "xor distance");
+  if constexpr (D == 1) return dpp<DPP_QP_XOR1>(v, v);
+  else if constexpr (D == 2) return dpp<DPP_QP_XOR2>(v, v);
+  else if constexpr (D == 8) return dpp<0x128>(v, v);  // row_ror:8
+  else if constexpr (D == 4 || D == 16) return __builtin_amdgcn_ds_swizzle(v, (D << 10) | 0x1F);
+  else return __shfl_xor(v, D);
+}
+
 // 64-bit max through cross-lane shuffles (used outside the hot loop).
 __device__ __forceinline__ int64_t wave_max64(int64_t v) {
 #pragma unroll
