@@ -3,6 +3,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <algorithm>
 #include <cstring>
 
 #include "fsched.h"
@@ -96,7 +97,9 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
   const int NP = next_pow2(n);
   const bool isjl = p->policy == FSCHED_ISJL;
   const int q_words = isjl ? NP / 2 : 0;
-  const int stage_words = p->policy != FSCHED_FCFS ? (Beff + 1) / 2 : 0;
+  // gather buffer (uint16 per worker), also the release scatter buffer (one
+  // word per 32 ranks)
+  const int stage_words = p->policy != FSCHED_FCFS ? std::max((Beff + 1) / 2, 64 * NW) : 0;
 
   fs::SimArgs a;
   std::memset(&a, 0, sizeof(a));

@@ -29,7 +29,7 @@ struct SimArgs {
   int32_t wave_words; // LDS words per wave
   int32_t off_arr;    // word offset of arrival-by-rank (general kernel)
   int32_t off_q;      // word offset of the plan-queue links (ISJL)
-  int32_t off_stage;  // word offset of the gather buffer (ISJL)
+  int32_t off_stage;  // word offset of the gather / release buffer (not FCFS)
   int32_t pad;
   const int32_t* arrival;
   const int32_t* prompt;

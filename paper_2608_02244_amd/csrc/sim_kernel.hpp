@@ -26,6 +26,7 @@
 //         ARR[r]   arrival of rank r (general variant only)
 //         QN[r]    next job in the same ISJL plan queue (uint16, ISJL)
 //         STG[j]   gather buffer of the first queued ranks (uint16, not FCFS)
+//         PEND[i]  released ranks on their way into the bitmap (aliases STG)
 //   The drain sweep sorts the active slots in registers and needs no LDS.
 //   VGPR  K worker slots per lane: worker w lives in slot w/64 of lane w%64
 //         (start, end, ISJL plan-queue head|tail); a bitmap of queued jobs over
@@ -186,13 +187,6 @@ struct PoolBits {
     }
     return -1;
   }
-  __device__ __forceinline__ void set(int r, int lane) {
-    int L = (r >> 5) & (WAVE - 1), wi = r >> 11;
-    uint32_t b = 1u << (r & 31);
-#pragma unroll
-    for (int i = 0; i < NW; ++i)
-      if (i == wi && lane == L) w[i] |= b;
-  }
   __device__ __forceinline__ void reset(int r, int lane) {
     int L = (r >> 5) & (WAVE - 1), wi = r >> 11;
     uint32_t b = 1u << (r & 31);
@@ -235,6 +229,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
   int32_t* ARR = (int32_t*)(W + a.off_arr);
   uint16_t* QN = (uint16_t*)(W + a.off_q);
   uint16_t* STG = (uint16_t*)(W + a.off_stage);
+  // Released ranks on their way into the bitmap (not FCFS); shares the gather
+  // buffer, which is dead while releases are processed.
+  uint32_t* PEND = W + a.off_stage;
   const int64_t row = inst * (int64_t)n;
   const int32_t* A = a.arrival + row;
   const int32_t* P = a.prompt + row;
@@ -246,19 +243,39 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
   }
 
   // ---- load, validate, instance constants --------------------------------
+  // One pass over the job table: validation, instance totals and the
+  // priority keys (LJF / ISJL: (-len, index); SJF: (len, index); FCFS:
+  // (arrival, index), or (len, index) in arrival order when arrivals are
+  // sorted); padding keys sort last.
+  const int NP = a.NP;
   int bad = 0, big = 0, unsorted = 0, maxlen = 0, maxarr = 0;
   int64_t osum = 0, qsum = 0, rsum = 0;
-  for (int i = lane; i < n; i += WAVE) {
-    int ar = A[i], p = P[i], o = O[i];
-    bad |= (ar < 0) | (p < 0) | (o < 1);
-    int64_t len = (int64_t)p + (int64_t)o;
-    big |= (len >= LEN_LIMIT);
-    if (i > 0) unsorted |= (A[i - 1] > ar);
-    if (len < LEN_LIMIT && len > maxlen) maxlen = (int)len;
-    if (ar > maxarr) maxarr = ar;
-    osum += len;
-    qsum += len * (len + 1) / 2;
-    rsum += ar;
+  int carry_ar = 0;
+  for (int i0 = 0; i0 < NP; i0 += WAVE) {
+    const int i = i0 + lane;
+    const bool in = i < n;
+    const int ar = in ? A[i] : 0x7FFFFFFF, p = in ? P[i] : 0, o = in ? O[i] : 1;
+    int prev = __shfl_up(ar, 1);
+    if (lane == 0) prev = i0 > 0 ? carry_ar : ar;
+    carry_ar = readlane(ar, WAVE - 1);
+    uint32_t key = 0xFFFFFFFFu;
+    if (in) {
+      bad |= (ar < 0) | (p < 0) | (o < 1);
+      const int64_t len = (int64_t)p + (int64_t)o;
+      big |= (len >= LEN_LIMIT);
+      unsorted |= (prev > ar);
+      if (len < LEN_LIMIT && len > maxlen) maxlen = (int)len;
+      if (ar > maxarr) maxarr = ar;
+      osum += len;
+      qsum += len * (len + 1) / 2;
+      rsum += ar;
+      const uint32_t l32 = (uint32_t)len & LMASK;
+      if (POL == POL_LJF || POL == POL_ISJL) key = ((LMASK - l32) << 12) | (uint32_t)i;
+      else if (POL == POL_SJF) key = (l32 << 12) | (uint32_t)i;
+      else if (GEN) key = (((uint32_t)ar & LMASK) << 12) | (uint32_t)i;
+      else key = (l32 << 12) | (uint32_t)i;
+    }
+    W[i] = key;
   }
   bad = ballot(bad != 0) != 0;
   big = ballot(big != 0) != 0;
@@ -302,21 +319,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
   }
 
   // ---- priority order -----------------------------------------------------
-  // LJF / ISJL: (-len, index); SJF: (len, index); FCFS: (arrival, index).
-  const int NP = a.NP;
-  if (POL == POL_FCFS && !GEN) {
-    for (int r = lane; r < n; r += WAVE) W[r] = ((uint32_t)(P[r] + O[r]) << 12) | (uint32_t)r;
-  } else {
-    for (int r = lane; r < NP; r += WAVE) {
-      uint32_t key = 0xFFFFFFFFu;
-      if (r < n) {
-        uint32_t len = (uint32_t)(P[r] + O[r]);
-        if (POL == POL_LJF || POL == POL_ISJL) key = ((LMASK - len) << 12) | (uint32_t)r;
-        else if (POL == POL_SJF) key = (len << 12) | (uint32_t)r;
-        else key = ((uint32_t)A[r] << 12) | (uint32_t)r;
-      }
-      W[r] = key;
-    }
+  if (!(POL == POL_FCFS && !GEN)) {
     wave_lds_sync();
     wave_bitonic_sort(W, NP, lane);
     for (int r = lane; r < n; r += WAVE) {
@@ -525,21 +528,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
     }
     if (S.ndone == n) break;
 
-    // (2) releases
-    if (POL == POL_FCFS) {
+    // (2) releases.  Arrivals are non-decreasing in job order here, so the
+    // jobs released by t are the next lanes of the loaded chunk up to the
+    // first later arrival; their pool bits are scattered with LDS atomics and
+    // folded into the register bitmap once.
+    if (POL == POL_FCFS || !GEN) {
+      bool any = false;
       while (relk < n) {
         if ((relk >> 6) != chunk) load_chunk(relk >> 6);
-        int rt = readlane(rel_t, relk & 63);
-        if (rt > t) break;
-        relk++;
+        const int off = relk & (WAVE - 1);
+        const uint64_t late = ballot(lane >= off && rel_t > t);
+        const int hi = late ? __builtin_ctzll(late) : WAVE;
+        if (POL != POL_FCFS && hi > off) {
+          if (!any) {
+#pragma unroll
+            for (int i = 0; i < NW; ++i) PEND[i * WAVE + lane] = 0u;
+            wave_lds_sync();
+            any = true;
+          }
+          if (lane >= off && lane < hi) atomicOr(&PEND[rel_r >> 5], 1u << (rel_r & 31));
+        }
+        relk += hi - off;
+        if (hi < WAVE) break;
       }
-    } else if (!GEN) {
-      while (relk < n) {
-        if ((relk >> 6) != chunk) load_chunk(relk >> 6);
-        int rt = readlane(rel_t, relk & 63);
-        if (rt > t) break;
-        pool.set(readlane(rel_r, relk & 63), lane);
-        relk++;
+      if (POL != POL_FCFS && any) {
+        wave_lds_sync();
+#pragma unroll
+        for (int i = 0; i < NW; ++i) pool.w[i] |= PEND[i * WAVE + lane];
+        wave_lds_sync();
       }
     } else if (next_rel <= t) {
       int nr = IDLE;
