@@ -134,6 +134,70 @@ __device__ inline void reg_bitonic_sort(uint32_t (&key)[K], int (&val)[K], int l
   }
 }
 
+// Lane-major register sort of 64 * KS keys: position p = lane * KS + k, so
+// the exchanges of distance below KS stay inside a lane and only the longer
+// ones cross lanes.  Ascending; keys only.
+template <int DK, int KS>
+__device__ __forceinline__ void lm_cx_regs(uint32_t (&key)[KS], int size, int lane) {
+  const bool lane_asc = ((lane * KS) & size) == 0;
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    if ((k & DK) == 0) {
+      const int h = k | DK;
+      const bool asc = lane_asc && (k & size) == 0;
+      const uint32_t x = key[k], y = key[h];
+      const uint32_t lo = min(x, y), hi = max(x, y);
+      key[k] = asc ? lo : hi;
+      key[h] = asc ? hi : lo;
+    }
+  }
+}
+
+template <int D, int KS>
+__device__ __forceinline__ void lm_cx_lanes(uint32_t (&key)[KS], int size, int lane) {
+  // distance D * KS >= KS: the block size exceeds KS, so the direction is the lane's
+  const bool take_min = ((lane & D) == 0) == (((lane * KS) & size) == 0);
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    const uint32_t pk = (uint32_t)shfl_xor_c<D>((int)key[k]);
+    key[k] = take_min ? min(key[k], pk) : max(key[k], pk);
+  }
+}
+
+// Sort W[0 .. 64*KS) ascending through registers (W is read in any order and
+// written back sorted).
+template <int KS>
+__device__ inline void wave_reg_sort(uint32_t* W, int lane) {
+  uint32_t key[KS];
+#pragma unroll
+  for (int k = 0; k < KS; ++k) key[k] = W[k * WAVE + lane];
+  for (int size = 2; size <= KS * WAVE; size <<= 1) {
+    for (int d = size >> 1; d > 0; d >>= 1) {
+      if (d < KS) {
+        switch (d) {
+          case 1: if constexpr (KS > 1) lm_cx_regs<1>(key, size, lane); break;
+          case 2: if constexpr (KS > 2) lm_cx_regs<2>(key, size, lane); break;
+          case 4: if constexpr (KS > 4) lm_cx_regs<4>(key, size, lane); break;
+          case 8: if constexpr (KS > 8) lm_cx_regs<8>(key, size, lane); break;
+          default: if constexpr (KS > 16) lm_cx_regs<16>(key, size, lane); break;
+        }
+      } else {
+        switch (d / KS) {
+          case 1: lm_cx_lanes<1>(key, size, lane); break;
+          case 2: lm_cx_lanes<2>(key, size, lane); break;
+          case 4: lm_cx_lanes<4>(key, size, lane); break;
+          case 8: lm_cx_lanes<8>(key, size, lane); break;
+          case 16: lm_cx_lanes<16>(key, size, lane); break;
+          default: lm_cx_lanes<32>(key, size, lane); break;
+        }
+      }
+    }
+  }
+  wave_lds_sync();
+#pragma unroll
+  for (int k = 0; k < KS; ++k) W[lane * KS + k] = key[k];
+}
+
 __device__ inline void write_marker(fsched_metrics* out, int64_t* out_T, int64_t inst,
                                     int64_t code, int lane) {
   if (lane == 0 && out_T) {
@@ -321,7 +385,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
   // ---- priority order -----------------------------------------------------
   if (!(POL == POL_FCFS && !GEN)) {
     wave_lds_sync();
-    wave_bitonic_sort(W, NP, lane);
+    switch (NP) {
+      case 64: wave_reg_sort<1>(W, lane); break;
+      case 128: wave_reg_sort<2>(W, lane); break;
+      case 256: wave_reg_sort<4>(W, lane); break;
+      case 512: wave_reg_sort<8>(W, lane); break;
+      case 1024: wave_reg_sort<16>(W, lane); break;
+      case 2048: wave_reg_sort<32>(W, lane); break;
+      default: wave_bitonic_sort(W, NP, lane); break;
+    }
+    wave_lds_sync();
     for (int r = lane; r < n; r += WAVE) {
       uint32_t key = W[r];
       int id = (int)(key & 0xFFFu);
