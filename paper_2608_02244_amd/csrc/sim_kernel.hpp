@@ -66,74 +66,6 @@ __device__ inline void wave_bitonic_sort(uint32_t* W, int NP, int lane) {
   }
 }
 
-// Compare-exchange of positions p and p ^ D (D < 64: lanes of one register)
-// in a bitonic stage of block `size`; position p = k * 64 + lane.  The payload
-// follows its key; equal keys keep their own payloads, which is a valid
-// outcome of the exchange.
-template <int D, int K>
-__device__ __forceinline__ void reg_cx_lanes(uint32_t (&key)[K], int (&val)[K], int size,
-                                             int lane) {
-  const bool lower = (lane & D) == 0;
-#pragma unroll
-  for (int k = 0; k < K; ++k) {
-    const uint32_t pk = (uint32_t)shfl_xor_c<D>((int)key[k]);
-    const int pv = shfl_xor_c<D>(val[k]);
-    const bool asc = ((k * WAVE + lane) & size) == 0;
-    const uint32_t nk = (lower == asc) ? min(key[k], pk) : max(key[k], pk);
-    val[k] = nk == key[k] ? val[k] : pv;
-    key[k] = nk;
-  }
-}
-
-// Compare-exchange of registers k and k ^ DK (distance DK * 64 positions).
-template <int DK, int K>
-__device__ __forceinline__ void reg_cx_regs(uint32_t (&key)[K], int (&val)[K], int size) {
-#pragma unroll
-  for (int k = 0; k < K; ++k) {
-    if ((k & DK) == 0) {
-      const int h = k | DK;
-      const bool asc = ((k * WAVE) & size) == 0;
-      const uint32_t x = key[k], y = key[h];
-      const int vx = val[k], vy = val[h];
-      const bool sw = (x > y) == asc;
-      key[k] = sw ? y : x;
-      key[h] = sw ? x : y;
-      val[k] = sw ? vy : vx;
-      val[h] = sw ? vx : vy;
-    }
-  }
-}
-
-// Bitonic sort, ascending, of the K * 64 keys held in registers (position
-// k * 64 + lane), each carrying one payload word.  No LDS is used.
-template <int K>
-__device__ inline void reg_bitonic_sort(uint32_t (&key)[K], int (&val)[K], int lane) {
-  for (int size = 2; size <= K * WAVE; size <<= 1) {
-    for (int d = size >> 1; d > 0; d >>= 1) {
-      switch (d) {
-        case 1: reg_cx_lanes<1>(key, val, size, lane); break;
-        case 2: reg_cx_lanes<2>(key, val, size, lane); break;
-        case 4: reg_cx_lanes<4>(key, val, size, lane); break;
-        case 8: reg_cx_lanes<8>(key, val, size, lane); break;
-        case 16: reg_cx_lanes<16>(key, val, size, lane); break;
-        case 32: reg_cx_lanes<32>(key, val, size, lane); break;
-        case 64:
-          if constexpr (K > 1) reg_cx_regs<1>(key, val, size);
-          break;
-        case 128:
-          if constexpr (K > 2) reg_cx_regs<2>(key, val, size);
-          break;
-        case 256:
-          if constexpr (K > 4) reg_cx_regs<4>(key, val, size);
-          break;
-        default:
-          if constexpr (K > 8) reg_cx_regs<8>(key, val, size);
-          break;
-      }
-    }
-  }
-}
-
 // Lane-major register sort of 64 * KS keys: position p = lane * KS + k, so
 // the exchanges of distance below KS stay inside a lane and only the longer
 // ones cross lanes.  Ascending; keys only.
@@ -161,6 +93,67 @@ __device__ __forceinline__ void lm_cx_lanes(uint32_t (&key)[KS], int size, int l
   for (int k = 0; k < KS; ++k) {
     const uint32_t pk = (uint32_t)shfl_xor_c<D>((int)key[k]);
     key[k] = take_min ? min(key[k], pk) : max(key[k], pk);
+  }
+}
+
+// The same network with one payload word per key (equal keys keep their own
+// payloads, a valid outcome of an exchange).
+template <int DK, int KS>
+__device__ __forceinline__ void lmp_cx_regs(uint32_t (&key)[KS], int (&val)[KS], int size,
+                                            int lane) {
+  const bool lane_asc = ((lane * KS) & size) == 0;
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    if ((k & DK) == 0) {
+      const int h = k | DK;
+      const bool asc = lane_asc && (k & size) == 0;
+      const uint32_t x = key[k], y = key[h];
+      const int vx = val[k], vy = val[h];
+      const bool sw = asc ? (x > y) : (x < y);
+      key[k] = sw ? y : x;
+      key[h] = sw ? x : y;
+      val[k] = sw ? vy : vx;
+      val[h] = sw ? vx : vy;
+    }
+  }
+}
+
+template <int D, int KS>
+__device__ __forceinline__ void lmp_cx_lanes(uint32_t (&key)[KS], int (&val)[KS], int size,
+                                             int lane) {
+  const bool take_min = ((lane & D) == 0) == (((lane * KS) & size) == 0);
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    const uint32_t pk = (uint32_t)shfl_xor_c<D>((int)key[k]);
+    const int pv = shfl_xor_c<D>(val[k]);
+    const uint32_t nk = take_min ? min(key[k], pk) : max(key[k], pk);
+    val[k] = nk == key[k] ? val[k] : pv;
+    key[k] = nk;
+  }
+}
+
+template <int KS>
+__device__ inline void reg_sort_payload(uint32_t (&key)[KS], int (&val)[KS], int lane) {
+  for (int size = 2; size <= KS * WAVE; size <<= 1) {
+    for (int d = size >> 1; d > 0; d >>= 1) {
+      if (d < KS) {
+        switch (d) {
+          case 1: if constexpr (KS > 1) lmp_cx_regs<1>(key, val, size, lane); break;
+          case 2: if constexpr (KS > 2) lmp_cx_regs<2>(key, val, size, lane); break;
+          case 4: if constexpr (KS > 4) lmp_cx_regs<4>(key, val, size, lane); break;
+          default: if constexpr (KS > 8) lmp_cx_regs<8>(key, val, size, lane); break;
+        }
+      } else {
+        switch (d / KS) {
+          case 1: lmp_cx_lanes<1>(key, val, size, lane); break;
+          case 2: lmp_cx_lanes<2>(key, val, size, lane); break;
+          case 4: lmp_cx_lanes<4>(key, val, size, lane); break;
+          case 8: lmp_cx_lanes<8>(key, val, size, lane); break;
+          case 16: lmp_cx_lanes<16>(key, val, size, lane); break;
+          default: lmp_cx_lanes<32>(key, val, size, lane); break;
+        }
+      }
+    }
   }
 }
 
@@ -992,7 +985,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
                           ((uint32_t)readlane((int)ws_q[0], 0) & 0xFFFFu) != QNONE;
     if ((POL == POL_LJF || (POL == POL_ISJL && mode == 1 && !w0_timer)) && S.nact > 0) {
       const int N = S.nact;
-      uint32_t dk[K];  // end - t of each active slot (inactive: all ones), sorted
+      // sorted position p = lane * K + k holds the p-th completion
+      uint32_t dk[K];  // end - t (inactive slots: all ones, sorted last)
       int dg[K];       // progress t - start, carried with its key
 #pragma unroll
       for (int k = 0; k < K; ++k) {
@@ -1000,101 +994,100 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
         dk[k] = act ? (uint32_t)(ws_end[k] - t) : 0xFFFFFFFFu;
         dg[k] = act ? t - ws_start[k] : 0;
       }
-      reg_bitonic_sort<K>(dk, dg, lane);
-      // One backward pass over the sorted positions, a register at a time
-      // (reversed so that lane L holds position k * 64 + 63 - L).  stop < 0:
-      // find the stop position (the lowest position ending a tie group after
-      // which the machine is empty or A_max <= alpha); otherwise accumulate
-      // the spans of the positions below `stop` and return the suffix state
-      // just after `stop`.
-      int64_t lE = 0, lC = 0, lW = 0, lX = 0, lB = 0, lU = 0, lP = 0;
-      int lXm = 0, lAm = 0;
-      int st_cnt = 0, st_g = 0, st_gmax = -1, st_gmin = IDLE, st_e = t;  // state after `stop`
-      auto pass = [&](int stop) -> int {
-        int c_cnt = 0, c_g = 0, c_gmin = IDLE, c_gmax = -1;
-        int found = N - 1;
-        for (int k = (N - 1) / WAVE; k >= 0; --k) {
-          // register k of the sorted keys (a select chain keeps the arrays in
-          // registers with a loop that is not unrolled)
-          int kc = 0, gc = 0, kn0 = 0;
+      reg_sort_payload<K>(dk, dg, lane);
+      // Suffix state of the lanes above this one (positions >= (lane+1)*K):
+      // progress sum, max and min.
+      int xs_g, xs_max, xs_min;
+      {
+        int lg = 0, lmx = -1, lmn = IDLE;
 #pragma unroll
-          for (int q = 0; q < K; ++q) {
-            if (q == k) {
-              kc = (int)dk[q];
-              gc = dg[q];
-            }
-            if (q == k + 1) kn0 = (int)dk[q];
+        for (int k = 0; k < K; ++k) {
+          if (lane * K + k < N) {
+            lg += dg[k];
+            lmx = max(lmx, dg[k]);
+            lmn = min(lmn, dg[k]);
           }
-          const int pos = k * WAVE + (WAVE - 1) - lane;
-          const bool valid = pos < N;
-          const int kr = __shfl(kc, (WAVE - 1) - lane);
-          const int gr = __shfl(gc, (WAVE - 1) - lane);
-          const int e = t + (valid ? kr : 0);
-          const int g = valid ? gr : 0;
-          int kn = __shfl_up(kr, 1);
-          if (lane == 0) kn = readlane(kn0, 0);
-          const int e_next = (pos + 1 < N) ? t + kn : e;
-          const int icnt = wave_scan_incl(valid ? 1 : 0);
-          const int ig = wave_scan_incl(g);
-          const int igmax = wave_scan_incl_max(valid ? g : (int)0x80000000);
-          const int igmin = wave_scan_incl_min(valid ? g : IDLE);
-          int pcnt = __shfl_up(icnt, 1), pg = __shfl_up(ig, 1);
-          int pgmax = __shfl_up(igmax, 1), pgmin = __shfl_up(igmin, 1);
-          if (lane == 0) {
-            pcnt = 0;
-            pg = 0;
-            pgmax = -1;
-            pgmin = IDLE;
-          }
-          const int cnt = c_cnt + pcnt;
-          const int gsum = c_g + pg;
-          const int gmax = max(c_gmax, pgmax), gmin = min(c_gmin, pgmin);
-          if (stop < 0) {
-            // A_max right after the completions at e: e - (t - gmax)
-            const bool group_end = valid && (pos + 1 >= N || e_next > e);
-            const bool ok = group_end && (cnt == 0 || e - t + gmax <= alpha);
-            const uint64_t mk = ballot(ok);
-            if (mk) found = min(found, k * WAVE + __builtin_clzll(mk));
-          } else {
-            const int64_t D = (int64_t)(e_next - e);
-            if (valid && pos < stop && D > 0) {
-              const int64_t s = cnt;
-              const int min_s = t - gmax, max_s = t - gmin;
-              const int64_t sum_s = s * (int64_t)t - gsum;
-              const int64_t m0 = (int64_t)(e - min_s) + 1;
-              const int64_t sm = D * m0 + D * (D - 1) / 2;
-              lE += D * (sum_s - s * (int64_t)min_s);
-              lC += a.c * D + a.tau * s * sm;
-              lW += a.c * D + a.tau * sm;
-              const int ext = max_s - min_s;
-              lX += D * ext;
-              lB += D;
-              if (ext > alpha) lU += D;
-              lXm = max(lXm, ext);
-              lAm = max(lAm, cnt);
-              lP = max(lP, s * (int64_t)e_next - sum_s);
-            }
-            const uint64_t hs = ballot(valid && pos == stop);
-            if (hs) {
-              const int L = __builtin_ctzll(hs);
-              st_cnt = readlane(cnt, L);
-              st_g = readlane(gsum, L);
-              st_gmax = readlane(gmax, L);
-              st_gmin = readlane(gmin, L);
-              st_e = readlane(e, L);
-            }
-          }
-          c_cnt += readlane(icnt, 63);
-          c_g += readlane(ig, 63);
-          c_gmax = max(c_gmax, readlane(igmax, 63));
-          c_gmin = min(c_gmin, readlane(igmin, 63));
         }
-        return found;
-      };
-      const int stop = (POL == POL_ISJL && planned > 0) ? pass(-1) : N - 1;
-      pass(stop);
-      const int tau_end = st_e;
-      // span [t, e_0): every job still active
+        const int incl = wave_scan_incl(lg);
+        xs_g = readlane(incl, WAVE - 1) - incl;
+        const int rmx = wave_scan_incl_max(__shfl(lmx, (WAVE - 1) - lane));
+        const int rmn = wave_scan_incl_min(__shfl(lmn, (WAVE - 1) - lane));
+        const int src = lane < WAVE - 1 ? (WAVE - 2) - lane : 0;
+        xs_max = __shfl(rmx, src);
+        xs_min = __shfl(rmn, src);
+        if (lane == WAVE - 1) {
+          xs_max = -1;
+          xs_min = IDLE;
+        }
+      }
+      // completion time of the first position of the next lane
+      const int e_up = t + (int)(uint32_t)__shfl_down((int)dk[0], 1);
+      // Stop position: the lowest position ending a tie group after which the
+      // machine is empty or A_max <= alpha (A_max right after the completions
+      // at e is e - t + the largest progress still active).
+      int stop = N - 1;
+      if (POL == POL_ISJL && planned > 0) {
+        int cg_max = xs_max, lfound = IDLE;
+#pragma unroll
+        for (int k = K - 1; k >= 0; --k) {
+          const int pos = lane * K + k;
+          const bool valid = pos < N;
+          const int e = t + (int)dk[k];
+          const int e_next = (k + 1 < K) ? t + (int)dk[k + 1 < K ? k + 1 : k] : e_up;
+          const bool group_end = valid && (pos + 1 >= N || e_next > e);
+          if (group_end && (pos + 1 >= N || e - t + cg_max <= alpha)) lfound = pos;
+          if (valid) cg_max = max(cg_max, dg[k]);
+        }
+        stop = min(stop, wave_min(lfound));
+      }
+      // Spans between consecutive completions below `stop`, each with the
+      // jobs at the positions above (count N - 1 - p, progress suffix sums).
+      int64_t lE = 0, lSM = 0, lSSM = 0, lX = 0, lP = 0;
+      int lU = 0;
+      int st_g = 0, st_gmax = -1, st_gmin = IDLE, st_e = 0;
+      {
+        int cg = xs_g, cg_max = xs_max, cg_min = xs_min;
+#pragma unroll
+        for (int k = K - 1; k >= 0; --k) {
+          const int pos = lane * K + k;
+          const bool valid = pos < N;
+          const int e = t + (int)dk[k];
+          const int e_next = (k + 1 < K) ? t + (int)dk[k + 1 < K ? k + 1 : k] : e_up;
+          if (valid && pos < stop && e_next > e) {
+            const int64_t D = (int64_t)(e_next - e);
+            const int64_t s = N - 1 - pos;
+            const int min_s = t - cg_max, max_s = t - cg_min;
+            const int64_t sum_s = s * (int64_t)t - cg;
+            const int64_t m0 = (int64_t)(e - min_s) + 1;
+            const int64_t sm = D * m0 + D * (D - 1) / 2;
+            lE += D * (sum_s - s * (int64_t)min_s);
+            lSM += sm;
+            lSSM += s * sm;
+            const int ext = max_s - min_s;
+            lX += D * ext;
+            if (ext > alpha) lU += (int)D;
+            lP = max(lP, s * (int64_t)e_next - sum_s);
+          }
+          if (pos == stop) {
+            st_g = cg;
+            st_gmax = cg_max;
+            st_gmin = cg_min;
+            st_e = e;
+          }
+          if (valid) {
+            cg += dg[k];
+            cg_max = max(cg_max, dg[k]);
+            cg_min = min(cg_min, dg[k]);
+          }
+        }
+      }
+      const int Ls = stop / K;
+      st_g = readlane(st_g, Ls);
+      st_gmax = readlane(st_gmax, Ls);
+      st_gmin = readlane(st_gmin, Ls);
+      const int tau_end = readlane(st_e, Ls);
+      // span [t, e_0): every job still active; the set only shrinks after it,
+      // so it also carries the largest extent and count of the sweep
       {
         const int e0 = t + readlane((int)dk[0], 0);
         const int64_t D = (int64_t)(e0 - t), s = N;
@@ -1102,26 +1095,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
         const int64_t sm = D * m0 + D * (D - 1) / 2;
         if (lane == 0) {
           lE += D * (S.sum_s - s * (int64_t)S.min_s);
-          lC += a.c * D + a.tau * s * sm;
-          lW += a.c * D + a.tau * sm;
+          lSM += sm;
+          lSSM += s * sm;
           const int ext = S.max_s - S.min_s;
           lX += D * ext;
-          lB += D;
-          if (ext > alpha) lU += D;
-          lXm = max(lXm, ext);
-          lAm = max(lAm, N);
+          if (ext > alpha) lU += (int)D;
           lP = max(lP, s * (int64_t)e0 - S.sum_s);
         }
+        acc_maxext = max(acc_maxext, S.max_s - S.min_s);
+        acc_maxact = max(acc_maxact, N);
       }
+      const int64_t span = (int64_t)(tau_end - t);
+      const int64_t sSM = wave_sum64(lSM), sSSM = wave_sum64(lSSM);
       acc_E += wave_sum64(lE);
-      acc_C += wave_sum64(lC);
-      acc_W += wave_sum64(lW);
+      acc_C += a.c * span + a.tau * sSSM;
+      acc_W += a.c * span + a.tau * sSM;
       acc_ext += wave_sum64(lX);
-      acc_busy += wave_sum64(lB);
-      acc_unfair += wave_sum64(lU);
+      acc_busy += span;
+      acc_unfair += wave_sum(lU);
       acc_peak = max(acc_peak, wave_max64(lP));
-      acc_maxext = max(acc_maxext, wave_max(lXm));
-      acc_maxact = max(acc_maxact, wave_max(lAm));
       // retire every job that completed by tau_end
       int rc = 0, rl = 0, me = IDLE;
 #pragma unroll
@@ -1140,7 +1132,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       S.nact = N - nret;
       S.min_end = wave_min(me);
       if (S.nact > 0) {
-        S.sum_s = (int64_t)st_cnt * t - st_g;
+        S.sum_s = (int64_t)S.nact * t - st_g;
         S.min_s = t - st_gmax;
         S.max_s = t - st_gmin;
       } else {

@@ -149,21 +149,43 @@ __device__ __forceinline__ int shfl_xor_c(int v) {
   else return __shfl_xor(v, D);
 }
 
-// 64-bit max through cross-lane shuffles (used outside the hot loop).
-__device__ __forceinline__ int64_t wave_max64(int64_t v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    int64_t o = __shfl_xor(v, off);
-    v = o > v ? o : v;
-  }
-  return uni64(v);
+// DPP move of a 64-bit value (both halves with the same control word).
+template <int CTRL, int ROW_MASK = 0xf, int BANK_MASK = 0xf>
+__device__ __forceinline__ uint64_t dpp64(uint64_t old, uint64_t src) {
+  const uint32_t lo = (uint32_t)dpp<CTRL, ROW_MASK, BANK_MASK>((int)(uint32_t)old, (int)(uint32_t)src);
+  const uint32_t hi = (uint32_t)dpp<CTRL, ROW_MASK, BANK_MASK>((int)(uint32_t)(old >> 32),
+                                                               (int)(uint32_t)(src >> 32));
+  return ((uint64_t)hi << 32) | lo;
 }
 
-// 64-bit sum through cross-lane shuffles (used outside the hot loop).
+__device__ __forceinline__ int64_t readlane64(int64_t v, int l) {
+  const uint32_t lo = (uint32_t)readlane((int)(uint32_t)v, l);
+  const uint32_t hi = (uint32_t)readlane((int)(uint32_t)((uint64_t)v >> 32), l);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// 64-bit max and sum, same DPP pattern as the 32-bit reductions.
+__device__ __forceinline__ int64_t wave_max64(int64_t v) {
+  uint64_t x = (uint64_t)v;
+  auto mx = [](uint64_t a, uint64_t b) { return (int64_t)a > (int64_t)b ? a : b; };
+  x = mx(x, dpp64<DPP_QP_XOR1>(x, x));
+  x = mx(x, dpp64<DPP_QP_XOR2>(x, x));
+  x = mx(x, dpp64<DPP_HALF_MIRROR>(x, x));
+  x = mx(x, dpp64<DPP_MIRROR>(x, x));
+  x = mx(x, dpp64<DPP_BCAST15, 0xa>(x, x));
+  x = mx(x, dpp64<DPP_BCAST31, 0xc>(x, x));
+  return readlane64((int64_t)x, 63);
+}
+
 __device__ __forceinline__ int64_t wave_sum64(int64_t v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-  return uni64(v);
+  uint64_t x = (uint64_t)v;
+  x += dpp64<DPP_QP_XOR1>(0, x);
+  x += dpp64<DPP_QP_XOR2>(0, x);
+  x += dpp64<DPP_HALF_MIRROR>(0, x);
+  x += dpp64<DPP_MIRROR>(0, x);
+  x += dpp64<DPP_BCAST15, 0xa>(0, x);
+  x += dpp64<DPP_BCAST31, 0xc>(0, x);
+  return readlane64((int64_t)x, 63);
 }
 
 // Order LDS accesses of this wave: all lanes of a wave issue LDS operations in
