@@ -157,13 +157,9 @@ __device__ inline void reg_sort_payload(uint32_t (&key)[KS], int (&val)[KS], int
   }
 }
 
-// Sort W[0 .. 64*KS) ascending through registers (W is read in any order and
-// written back sorted).
+// Sort the 64 * KS keys held in registers, ascending in lane-major order.
 template <int KS>
-__device__ inline void wave_reg_sort(uint32_t* W, int lane) {
-  uint32_t key[KS];
-#pragma unroll
-  for (int k = 0; k < KS; ++k) key[k] = W[k * WAVE + lane];
+__device__ inline void reg_sort_keys(uint32_t (&key)[KS], int lane) {
   for (int size = 2; size <= KS * WAVE; size <<= 1) {
     for (int d = size >> 1; d > 0; d >>= 1) {
       if (d < KS) {
@@ -186,6 +182,16 @@ __device__ inline void wave_reg_sort(uint32_t* W, int lane) {
       }
     }
   }
+}
+
+// Sort W[0 .. 64*KS) ascending through registers (W is read in any order and
+// written back sorted).
+template <int KS>
+__device__ inline void wave_reg_sort(uint32_t* W, int lane) {
+  uint32_t key[KS];
+#pragma unroll
+  for (int k = 0; k < KS; ++k) key[k] = W[k * WAVE + lane];
+  reg_sort_keys<KS>(key, lane);
   wave_lds_sync();
 #pragma unroll
   for (int k = 0; k < KS; ++k) W[lane * KS + k] = key[k];
@@ -988,13 +994,33 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       // sorted position p = lane * K + k holds the p-th completion
       uint32_t dk[K];  // end - t (inactive slots: all ones, sorted last)
       int dg[K];       // progress t - start, carried with its key
+      // Progress is at most t - min_s and end - t at most the longest job:
+      // when both fit one word together the progress rides in the low bits
+      // of the key and the sort moves keys only.
+      const int gbits = 32 - __builtin_clz((uint32_t)(t - S.min_s) | 1u);
+      if (gbits < 32 && (int64_t)maxlen < (int64_t)(0xFFFFFFFFu >> gbits)) {
 #pragma unroll
-      for (int k = 0; k < K; ++k) {
-        const bool act = ws_end[k] != IDLE;
-        dk[k] = act ? (uint32_t)(ws_end[k] - t) : 0xFFFFFFFFu;
-        dg[k] = act ? t - ws_start[k] : 0;
+        for (int k = 0; k < K; ++k) {
+          const bool act = ws_end[k] != IDLE;
+          dk[k] = act ? ((uint32_t)(ws_end[k] - t) << gbits) | (uint32_t)(t - ws_start[k])
+                      : 0xFFFFFFFFu;
+        }
+        reg_sort_keys<K>(dk, lane);
+        const uint32_t gmask = (1u << gbits) - 1u;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          dg[k] = (int)(dk[k] & gmask);
+          dk[k] = dk[k] == 0xFFFFFFFFu ? 0xFFFFFFFFu : dk[k] >> gbits;
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const bool act = ws_end[k] != IDLE;
+          dk[k] = act ? (uint32_t)(ws_end[k] - t) : 0xFFFFFFFFu;
+          dg[k] = act ? t - ws_start[k] : 0;
+        }
+        reg_sort_payload<K>(dk, dg, lane);
       }
-      reg_sort_payload<K>(dk, dg, lane);
       // Suffix state of the lanes above this one (positions >= (lane+1)*K):
       // progress sum, max and min.
       int xs_g, xs_max, xs_min;
