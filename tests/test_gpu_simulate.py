@@ -261,3 +261,20 @@ def test_named_workloads_full_size(dev, name):
             assert_same(ctx + " (schedules)", gm, ref, gs, rs, gf, rf)
     del ta, tp, to
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("policy", ["isjl", "ljf"])
+def test_long_jobs(dev, policy):
+    """Lengths close to 2^20: the drain sweep cannot pack progress under the
+    completion key and takes the payload sort."""
+    rng = np.random.default_rng(zlib.crc32(f"long:{policy}".encode()))
+    n = 40
+    for B, alpha in ((3, 1000), (8, 200000), (5, 0)):
+        o = rng.integers(1, (1 << 20) - 1, size=(4, n)).astype(np.int32)
+        o[:, ::3] = rng.integers(1, 5000, size=o[:, ::3].shape)  # mix in short jobs
+        p = np.zeros_like(o)
+        a = np.sort(rng.integers(0, 1 << 19, size=(4, n)), axis=1).astype(np.int32)
+        a[:2] = 0
+        log(f"long jobs {policy} B={B} alpha={alpha}")
+        check(dev, f"long {policy} B={B} alpha={alpha}", a, p, o, policy=policy, B=B,
+              alpha=alpha, M_kv=0, cost_c=3, cost_tau=1)
