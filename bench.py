@@ -77,10 +77,14 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", default="simulate", choices=["simulate", "copy", "decompose", "opt"],
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the per-alpha roofline lines of the fairness-budget sweep workload")
+    ap.add_argument("--mode", default="simulate",
+                    choices=["simulate", "copy", "decompose", "opt", "host"],
                     help="simulate: the benchmark line; copy: a plain device copy of known size "
                          "(calibrates the HBM byte counters); decompose / opt: time the other "
-                         "two library calls (for profiles)")
+                         "two library calls (for profiles); host: host-buffer calls, "
+                         "PCIe copies included")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the instances are "
@@ -99,6 +103,8 @@ def main() -> int:
         return time_decompose(torch, np, workload, fs, args)
     if args.mode == "opt":
         return time_opt(torch, np, workload, fs, args)
+    if args.mode == "host":
+        return time_host(torch, np, workload, fs, args)
     w = workload.WORKLOADS[args.workload]
     alpha = w.alphas[0]
     policy = "isjl"
@@ -154,6 +160,9 @@ def main() -> int:
                       "instance_steps_per_step": inst_steps, "generate_s": round(gen_s, 3)},
            "roofline": roofline}
 
+    if not args.no_sweep:
+        out["alpha_sweep"] = alpha_sweep(torch, np, workload, fs, stream)
+
     if not args.no_cpu_baseline:
         import oracle
         kw_o = dict(policy=policy, B=w.B, alpha=alpha, M_kv=w.M_kv, cost_c=w.cost_c,
@@ -173,6 +182,59 @@ def main() -> int:
                                          f"{cpu_s:.1f} s",
                                "parity_on_sample": parity}
     print(json.dumps(out), flush=True)
+    return 0
+
+
+def alpha_sweep(torch, np, workload, fs, stream, reps: int = 5) -> dict:
+    """ISJL over the fairness-budget sweep workload (4,096 instances x 2,000 jobs,
+    B = 128, M_kv = 262,144), one launch per alpha: instance-steps/s and the
+    fraction of the ALU roofline, kernel time from HIP events (median of reps)."""
+    w = workload.WORKLOADS["bimodal_sweep_4096x2000"]
+    a, p, o = workload.generate(w)
+    sorted_arrivals = bool((np.diff(a, axis=1) >= 0).all())
+    ta, tp, to = (torch.from_numpy(x).to("cuda:0") for x in (a, p, o))
+    ops = algorithmic_ops(w.n_inst, w.n_jobs, w.B, "isjl", sorted_arrivals)
+    rows = []
+    for al in w.alphas:
+        kw = dict(policy="isjl", B=w.B, alpha=al, M_kv=w.M_kv, cost_c=w.cost_c,
+                  cost_tau=w.cost_tau)
+        raw, _, _ = fs.simulate(ta, tp, to, **kw)
+        torch.cuda.synchronize()
+        steps = int(fs.metrics_view(raw)["T"].sum())
+        ms = []
+        for _ in range(reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fs.simulate(ta, tp, to, **kw)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        t = sorted(ms)[len(ms) // 2] / 1e3
+        rows.append({"alpha": "inf" if al == workload.ALPHA_INF else al, "ms": t * 1e3,
+                     "instance_steps_per_s": steps / t, "frac": ops / t / PEAK_ALU})
+    return {"workload": w.name, "policy": "isjl", "B": w.B, "M_kv": w.M_kv,
+            "ops_per_launch": ops, "bound": "alu", "results": rows}
+
+
+def time_host(torch, np, workload, fs, args) -> int:
+    """Host-buffer calls (the library stages the tables to the device and the
+    metrics back): end-to-end rate including the PCIe copies."""
+    w = workload.WORKLOADS[args.workload]
+    a, p, o = workload.generate(w)
+    kw = dict(policy="isjl", B=w.B, alpha=w.alphas[0], M_kv=w.M_kv, cost_c=w.cost_c,
+              cost_tau=w.cost_tau)
+    raw, _, _ = fs.simulate(a, p, o, **kw)
+    steps = int(fs.metrics_view(raw)["T"].sum())
+    for _ in range(args.warmup):
+        fs.simulate(a, p, o, **kw)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        fs.simulate(a, p, o, **kw)
+    dt = (time.perf_counter() - t0) / args.steps
+    print(json.dumps({"mode": "host", "workload": w.name, "ms_per_call": dt * 1e3,
+                      "instance_steps_per_s": steps / dt,
+                      "table_bytes": int(a.nbytes + p.nbytes + o.nbytes)}))
     return 0
 
 

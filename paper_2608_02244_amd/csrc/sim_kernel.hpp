@@ -436,6 +436,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
     }
   }
   int relk = 0;           // release cursor
+  int qcount = 0;         // queued jobs: released, not admitted, not planned
   int chunk = -1;         // release chunk loaded in rel_t / rel_r
   int rel_t = IDLE, rel_r = 0;
   int next_rel = 0;       // general variant, non-FCFS
@@ -525,6 +526,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
   auto admit_prefix = [&](int t, int G, bool need_empty_queue, int& adm, int64_t& adm_len,
                           int& adm_minlen) -> int {
     int na = G;
+    int64_t tot64 = -1;  // summed length of the admitted jobs, when the KV scan found it
     if (M != 0) {
       int64_t run = S.res;
       for (int c0 = 0; c0 < G; c0 += WAVE) {
@@ -534,14 +536,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
         const bool fail = j < G && (j > 0 || S.nact > 0) && (run + pre > M);
         const uint64_t fm = ballot(fail);
         if (fm) {
-          na = c0 + __builtin_ctzll(fm);
+          const int f = __builtin_ctzll(fm);
+          na = c0 + f;
+          if (f > 0) run += readlane(pre, f - 1);
           break;
         }
         run += readlane(pre, 63);
       }
+      tot64 = run - S.res;
     }
     if (na == 0) return 0;
-    int base = 0, lsum = 0, lmin = IDLE;
+    int base = 0, lsum = 0;
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       if (base < na) {
@@ -556,14 +561,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
           ws_end[k] = t + len;
           emit(pid(wv), t, len);
           lsum += len;
-          lmin = min(lmin, len);
         }
         base += __builtin_popcountll(bm);
       }
     }
-    const int tot = wave_sum(lsum);
-    adm_minlen = min(adm_minlen, wave_min(lmin));
+    const int tot = tot64 >= 0 ? (int)tot64 : wave_sum(lsum);
+    // the gathered jobs are in priority order, so the shortest admitted one is
+    // the last (longest first) or the first (SJF)
+    adm_minlen = min(adm_minlen, plen(W[STG[POL == POL_SJF ? 0 : na - 1]]));
     pool.clear_upto(STG[na - 1], lane);  // the first na queued ranks
+    qcount -= na;
     adm += na;
     adm_len += tot;
     S.res += tot;
@@ -575,24 +582,38 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
     const int t = S.t;
     // (1) retire the jobs whose last token was processed at t-1
     if (S.min_end == t) {
-      int cnt = 0, lsum = 0, me = IDLE, mn = IDLE, mx = -1;
+      // the earliest / latest start is searched again only if a job holding
+      // it retires
+      int nret = 0, lsum = 0, me = IDLE;
+      bool hmin = false, hmax = false;
 #pragma unroll
       for (int k = 0; k < K; ++k) {
-        if (ws_end[k] == t) {
-          cnt++;
+        const bool r = ws_end[k] == t;
+        nret += __builtin_popcountll(ballot(r));
+        if (r) {
           lsum += ws_end[k] - ws_start[k];
+          hmin |= ws_start[k] == S.min_s;
+          hmax |= ws_start[k] == S.max_s;
           ws_end[k] = IDLE;
           ws_start[k] = IDLE;
         }
         me = min(me, ws_end[k]);
-        mn = min(mn, ws_start[k]);
-        if (ws_start[k] != IDLE) mx = max(mx, ws_start[k]);
       }
-      int nret = wave_sum(cnt);
       int lret = wave_sum(lsum);
       S.min_end = wave_min(me);
-      S.min_s = wave_min(mn);
-      S.max_s = wave_max(mx);
+      if (ballot(hmin)) {
+        int mn = IDLE;
+#pragma unroll
+        for (int k = 0; k < K; ++k) mn = min(mn, ws_start[k]);
+        S.min_s = wave_min(mn);
+      }
+      if (ballot(hmax)) {
+        int mx = -1;
+#pragma unroll
+        for (int k = 0; k < K; ++k)
+          if (ws_start[k] != IDLE) mx = max(mx, ws_start[k]);
+        S.max_s = wave_max(mx);
+      }
       S.ndone += nret;
       S.nact -= nret;
       S.res -= lret;
@@ -619,6 +640,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
             any = true;
           }
           if (lane >= off && lane < hi) atomicOr(&PEND[rel_r >> 5], 1u << (rel_r & 31));
+          qcount += hi - off;
         }
         relk += hi - off;
         if (hi < WAVE) break;
@@ -630,7 +652,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
         wave_lds_sync();
       }
     } else if (next_rel <= t) {
-      int nr = IDLE;
+      int nr = IDLE, ng = 0;
 #pragma unroll
       for (int i = 0; i < NW; ++i) {
         uint32_t u = unrel.w[i], got = 0u;
@@ -644,7 +666,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
         }
         unrel.w[i] &= ~got;
         pool.w[i] |= got;
+        ng += __builtin_popcount(got);
       }
+      qcount += wave_sum(ng);
       next_rel = wave_min(nr);
     }
 
@@ -703,7 +727,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       if (POL == POL_SJF || S.nact == 0) {
         const int freew = Beff - S.nact;
         if (freew > 0) {
-          const int kp = pool.count();
+          const int kp = qcount;
           const int G = min(freew, kp);
           if (G > 0) {
             gather_first(G);
@@ -714,7 +738,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
     } else {  // ISJL
       // Epoch: empty machine, nothing planned, jobs queued -> Phase ONE.
       if (S.nact == 0 && planned == 0) {
-        int kp = pool.count();
+        int kp = qcount;
         if (kp > 0) {
           mode = 0;
           int G = min(Beff, kp);
@@ -764,6 +788,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
             // the m long jobs are the first m queued ranks
             const int rlast = STG[m - 1];
             pool.clear_upto(rlast, lane);
+            qcount -= m;
             planned += m;
             // Pack scan (Algorithm 3): remaining queued jobs in decreasing length;
             // each goes to the first spare worker with room, else to the long
@@ -844,6 +869,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
                   ws_q[k] = h | ((uint32_t)r << 16);
                 }
               pool.reset(r, lane);
+              --qcount;
               planned++;
               cur = r;
             }
@@ -946,14 +972,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       // Phase TWO (FILL): idle workers with nothing planned take the longest
       // queued unplanned job while A_max(t) <= alpha; otherwise DRAIN.
       if (mode == 0) {
-        int ie = 0;
+        // idle workers with an empty plan queue (all idle ones when nothing is planned)
+        int nie = Beff - S.nact;
+        if (planned > 0) {
+          nie = 0;
 #pragma unroll
-        for (int k = 0; k < K; ++k)
-          ie += (valid[k] && ws_end[k] == IDLE && (ws_q[k] & 0xFFFFu) == QNONE) ? 1 : 0;
-        const int nie = wave_sum(ie);
+          for (int k = 0; k < K; ++k)
+            nie += __builtin_popcountll(
+                ballot(valid[k] && ws_end[k] == IDLE && (ws_q[k] & 0xFFFFu) == QNONE));
+        }
         free_empty = nie;
         if (nie > 0) {
-          const int kp = pool.count();
+          const int kp = qcount;
           if (kp > 0) {
             if (amax > alpha) {
               mode = 1;
