@@ -96,7 +96,9 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
   const int NW = n <= 2048 ? 1 : 2;
   const int NP = next_pow2(n);
   const bool isjl = p->policy == FSCHED_ISJL;
-  const int q_words = isjl ? NP / 2 : 0;
+  // plan-queue links; with alpha = infinity Phase ONE never plans (no second
+  // job is longer than alpha), so the links are not needed
+  const int q_words = (isjl && p->alpha != FSCHED_ALPHA_INF) ? NP / 2 : 0;
   // gather buffer (uint16 per worker), also the release scatter buffer (one
   // word per 32 ranks)
   const int stage_words = p->policy != FSCHED_FCFS ? std::max((Beff + 1) / 2, 64 * NW) : 0;
