@@ -799,33 +799,44 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
           mode = 0;
           int G = min(Beff, kp);
           gather_first(G);  // longest first
+          // lengths of the gathered jobs: job j in chunk j / 64, lane j % 64
+          // (worker w's long job is gathered job w, in the same place)
+          int glen[K];
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            const int j = k * WAVE + lane;
+            glen[k] = j < G ? plen(W[STG[j]]) : 0;
+          }
           // Bp: largest prefix of the longest jobs that fits the KV budget
           int Bp = G;
           if (M != 0) {
             int64_t run = 0;
-            for (int c0 = 0; c0 < G; c0 += WAVE) {
-              int j = c0 + lane;
-              int len = j < G ? plen(W[STG[j]]) : 0;
-              int pre = wave_scan_incl(len);
-              uint64_t fm = ballot(j < G && j >= 1 && run + pre > M);
-              if (fm) {
-                Bp = c0 + __builtin_ctzll(fm);
-                break;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              if (k * WAVE < G && Bp == G) {
+                const int j = k * WAVE + lane;
+                const int pre = wave_scan_incl(glen[k]);
+                const uint64_t fm = ballot(j < G && j >= 1 && run + pre > M);
+                if (fm) Bp = k * WAVE + __builtin_ctzll(fm);
+                else run += readlane(pre, 63);
               }
-              run += readlane(pre, 63);
             }
             if (Bp < 1) Bp = 1;
           }
-          int o2 = kp > 1 ? plen(W[STG[1]]) : 0;
+          const int o1 = readlane(glen[0], 0);
+          const int o2 = kp > 1 ? readlane(glen[0], 1) : 0;
           if (kp > 1 && Bp > 1 && o2 > alpha) {
-            // M = min{Bp, #{len > alpha}} (a prefix of the sorted queue)
-            int m = 0;
-            for (int c0 = 0; c0 < Bp; c0 += WAVE) {
-              int j = c0 + lane;
-              bool lng = j < Bp && plen(W[STG[j]]) > alpha;
-              m += __builtin_popcountll(ballot(lng));
+            // m = min{Bp, #{len > alpha}}: the lengths are non-increasing, so it
+            // is the first gathered job with len <= alpha, capped at Bp
+            int m = Bp;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              if (k * WAVE < Bp && m == Bp) {
+                const int j = k * WAVE + lane;
+                const uint64_t fm = ballot(j < Bp && glen[k] <= alpha);
+                if (fm) m = min(Bp, k * WAVE + __builtin_ctzll(fm));
+              }
             }
-            const int o1 = plen(W[STG[0]]);
             const int beta = a.beta;
             int cap[K], load[K];
 #pragma unroll
@@ -833,8 +844,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
               int w = k * WAVE + lane;
               load[k] = 0;
               if (w >= 1 && w < m) {
-                int lj = plen(W[STG[w]]);
-                cap[k] = min(2 * alpha, o1 - lj + beta);
+                cap[k] = min(2 * alpha, o1 - glen[k] + beta);
               } else if (w >= m && w < Bp) {
                 cap[k] = alpha;
               } else {
