@@ -1082,10 +1082,33 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
     // positions > i (their count, progress sum and progress range are suffix
     // scans).  The sweep stops at the first completion after which a planned
     // job could start; the jobs still active there stay in their slots.
+    // The same holds for FCFS, SJF and ISJL in FILL with nothing queued or
+    // planned: no completion before the next release carries a decision, so
+    // those completions are swept too (when there are a few of them).
     const bool w0_timer = POL == POL_ISJL && planned > 0 && t_w1 > t &&
                           readlane(ws_end[0], 0) == IDLE &&
                           ((uint32_t)readlane((int)ws_q[0], 0) & 0xFFFFu) != QNONE;
-    if ((POL == POL_LJF || (POL == POL_ISJL && mode == 1 && !w0_timer)) && S.nact > 0) {
+    int quiet = 0;  // completions up to the next release, when nothing waits
+    if (POL != POL_LJF && S.nact > 0 &&
+        (POL == POL_FCFS ? head == relk
+                         : (qcount == 0 && (POL != POL_ISJL || (mode == 0 && planned == 0))))) {
+      int r_next = IDLE;
+      if (POL == POL_FCFS || !GEN) {
+        if (relk < n) {
+          if ((relk >> 6) != chunk) load_chunk(relk >> 6);
+          r_next = readlane(rel_t, relk & (WAVE - 1));
+        }
+      } else {
+        r_next = next_rel;
+      }
+      if (S.min_end <= r_next) {
+#pragma unroll
+        for (int k = 0; k < K; ++k)
+          quiet += __builtin_popcountll(ballot(ws_end[k] != IDLE && ws_end[k] <= r_next));
+      }
+    }
+    if ((POL == POL_LJF || (POL == POL_ISJL && mode == 1 && !w0_timer) || quiet >= 3) &&
+        S.nact > 0) {
       const int N = S.nact;
       // sorted position p = lane * K + k holds the p-th completion
       uint32_t dk[K];  // end - t (inactive slots: all ones, sorted last)
@@ -1147,7 +1170,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       // Stop position: the lowest position ending a tie group after which the
       // machine is empty or A_max <= alpha (A_max right after the completions
       // at e is e - t + the largest progress still active).
-      int stop = N - 1;
+      int stop = quiet >= 3 ? quiet - 1 : N - 1;
       if (POL == POL_ISJL && planned > 0) {
         int cg_max = xs_max, lfound = IDLE;
 #pragma unroll
