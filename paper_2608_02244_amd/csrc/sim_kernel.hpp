@@ -33,6 +33,8 @@
 //         ranks (bit r%32 of word r/2048 in lane (r/32)%64).
 //   SGPR  time, counters, cost accumulators.
 #pragma once
+#include <type_traits>
+
 #include "sim_common.hpp"
 #include "wave.hpp"
 
@@ -1107,134 +1109,165 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
           quiet += __builtin_popcountll(ballot(ws_end[k] != IDLE && ws_end[k] <= r_next));
       }
     }
-    if ((POL == POL_LJF || (POL == POL_ISJL && mode == 1 && !w0_timer) || quiet >= 3) &&
-        S.nact > 0) {
+    bool sweep = (POL == POL_LJF || (POL == POL_ISJL && mode == 1 && !w0_timer) || quiet >= 3) &&
+                 S.nact > 0;
+    if (sweep) {
       const int N = S.nact;
-      // sorted position p = lane * K + k holds the p-th completion
-      uint32_t dk[K];  // end - t (inactive slots: all ones, sorted last)
-      int dg[K];       // progress t - start, carried with its key
       // Progress is at most t - min_s and end - t at most the longest job:
       // when both fit one word together the progress rides in the low bits
       // of the key and the sort moves keys only.
       const int gbits = 32 - __builtin_clz((uint32_t)(t - S.min_s) | 1u);
-      if (gbits < 32 && (int64_t)maxlen < (int64_t)(0xFFFFFFFFu >> gbits)) {
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-          const bool act = ws_end[k] != IDLE;
-          dk[k] = act ? ((uint32_t)(ws_end[k] - t) << gbits) | (uint32_t)(t - ws_start[k])
-                      : 0xFFFFFFFFu;
-        }
-        reg_sort_keys<K>(dk, lane);
-        const uint32_t gmask = (1u << gbits) - 1u;
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-          dg[k] = (int)(dk[k] & gmask);
-          dk[k] = dk[k] == 0xFFFFFFFFu ? 0xFFFFFFFFu : dk[k] >> gbits;
-        }
-      } else {
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-          const bool act = ws_end[k] != IDLE;
-          dk[k] = act ? (uint32_t)(ws_end[k] - t) : 0xFFFFFFFFu;
-          dg[k] = act ? t - ws_start[k] : 0;
-        }
-        reg_sort_payload<K>(dk, dg, lane);
-      }
-      // Suffix state of the lanes above this one (positions >= (lane+1)*K):
-      // progress sum, max and min.
-      int xs_g, xs_max, xs_min;
-      {
-        int lg = 0, lmx = -1, lmn = IDLE;
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-          if (lane * K + k < N) {
-            lg += dg[k];
-            lmx = max(lmx, dg[k]);
-            lmn = min(lmn, dg[k]);
-          }
-        }
-        const int incl = wave_scan_incl(lg);
-        xs_g = readlane(incl, WAVE - 1) - incl;
-        const int rmx = wave_scan_incl_max(__shfl(lmx, (WAVE - 1) - lane));
-        const int rmn = wave_scan_incl_min(__shfl(lmn, (WAVE - 1) - lane));
-        const int src = lane < WAVE - 1 ? (WAVE - 2) - lane : 0;
-        xs_max = __shfl(rmx, src);
-        xs_min = __shfl(rmn, src);
-        if (lane == WAVE - 1) {
-          xs_max = -1;
-          xs_min = IDLE;
-        }
-      }
-      // completion time of the first position of the next lane
-      const int e_up = t + (int)(uint32_t)__shfl_down((int)dk[0], 1);
-      // Stop position: the lowest position ending a tie group after which the
-      // machine is empty or A_max <= alpha (A_max right after the completions
-      // at e is e - t + the largest progress still active).
-      int stop = quiet >= 3 ? quiet - 1 : N - 1;
-      if (POL == POL_ISJL && planned > 0) {
-        int cg_max = xs_max, lfound = IDLE;
-#pragma unroll
-        for (int k = K - 1; k >= 0; --k) {
-          const int pos = lane * K + k;
-          const bool valid = pos < N;
-          const int e = t + (int)dk[k];
-          const int e_next = (k + 1 < K) ? t + (int)dk[k + 1 < K ? k + 1 : k] : e_up;
-          const bool group_end = valid && (pos + 1 >= N || e_next > e);
-          if (group_end && (pos + 1 >= N || e - t + cg_max <= alpha)) lfound = pos;
-          if (valid) cg_max = max(cg_max, dg[k]);
-        }
-        stop = min(stop, wave_min(lfound));
-      }
-      // Spans between consecutive completions below `stop`, each with the
-      // jobs at the positions above (count N - 1 - p, progress suffix sums).
+      const bool packed = gbits < 32 && (int64_t)maxlen < (int64_t)(0xFFFFFFFFu >> gbits);
+      int stop = 0, e0 = 0, st_g = 0, st_gmax = -1, st_gmin = IDLE, tau_end = 0;
       int64_t lE = 0, lSM = 0, lSSM = 0, lX = 0, lP = 0;
       int lU = 0;
-      int st_g = 0, st_gmax = -1, st_gmin = IDLE, st_e = 0;
-      {
-        int cg = xs_g, cg_max = xs_max, cg_min = xs_min;
+      // Sort the N completions into KS registers per lane (position
+      // p = lane * KS + k holds the p-th) and account the spans.  KS = K sorts
+      // every slot in place; KS = 1 first packs up to 64 active slots into one
+      // register through the gather buffer (for K >= 4).
+      auto sweep_body = [&](auto ks_tag) {
+        constexpr int KS = decltype(ks_tag)::value;
+        uint32_t dk[KS];  // end - t (unused positions: all ones, sorted last)
+        int dg[KS];       // progress t - start, carried with its key
+        if (packed) {
+          if constexpr (KS == K) {
 #pragma unroll
-        for (int k = K - 1; k >= 0; --k) {
-          const int pos = lane * K + k;
-          const bool valid = pos < N;
-          const int e = t + (int)dk[k];
-          const int e_next = (k + 1 < K) ? t + (int)dk[k + 1 < K ? k + 1 : k] : e_up;
-          if (valid && pos < stop && e_next > e) {
-            const int64_t D = (int64_t)(e_next - e);
-            const int64_t s = N - 1 - pos;
-            const int min_s = t - cg_max, max_s = t - cg_min;
-            const int64_t sum_s = s * (int64_t)t - cg;
-            const int64_t m0 = (int64_t)(e - min_s) + 1;
-            const int64_t sm = D * m0 + D * (D - 1) / 2;
-            lE += D * (sum_s - s * (int64_t)min_s);
-            lSM += sm;
-            lSSM += s * sm;
-            const int ext = max_s - min_s;
-            lX += D * ext;
-            if (ext > alpha) lU += (int)D;
-            lP = max(lP, s * (int64_t)e_next - sum_s);
+            for (int k = 0; k < K; ++k) {
+              const bool act = ws_end[k] != IDLE;
+              dk[k] = act ? ((uint32_t)(ws_end[k] - t) << gbits) | (uint32_t)(t - ws_start[k])
+                          : 0xFFFFFFFFu;
+            }
+          } else {
+            int base = 0;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              const bool act = ws_end[k] != IDLE;
+              const uint64_t bm = ballot(act);
+              if (act)
+                PEND[base + mbcnt(bm)] =
+                    ((uint32_t)(ws_end[k] - t) << gbits) | (uint32_t)(t - ws_start[k]);
+              base += __builtin_popcountll(bm);
+            }
+            wave_lds_sync();
+            dk[0] = lane < N ? PEND[lane] : 0xFFFFFFFFu;
+            wave_lds_sync();
           }
-          if (pos == stop) {
-            st_g = cg;
-            st_gmax = cg_max;
-            st_gmin = cg_min;
-            st_e = e;
+          reg_sort_keys<KS>(dk, lane);
+          const uint32_t gmask = (1u << gbits) - 1u;
+#pragma unroll
+          for (int k = 0; k < KS; ++k) {
+            dg[k] = (int)(dk[k] & gmask);
+            dk[k] = dk[k] == 0xFFFFFFFFu ? 0xFFFFFFFFu : dk[k] >> gbits;
           }
-          if (valid) {
-            cg += dg[k];
-            cg_max = max(cg_max, dg[k]);
-            cg_min = min(cg_min, dg[k]);
+        } else if constexpr (KS == K) {
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            const bool act = ws_end[k] != IDLE;
+            dk[k] = act ? (uint32_t)(ws_end[k] - t) : 0xFFFFFFFFu;
+            dg[k] = act ? t - ws_start[k] : 0;
+          }
+          reg_sort_payload<K>(dk, dg, lane);
+        }
+        // Suffix state of the lanes above this one (positions >= (lane+1)*KS):
+        // progress sum, max and min.
+        int xs_g, xs_max, xs_min;
+        {
+          int lg = 0, lmx = -1, lmn = IDLE;
+#pragma unroll
+          for (int k = 0; k < KS; ++k) {
+            if (lane * KS + k < N) {
+              lg += dg[k];
+              lmx = max(lmx, dg[k]);
+              lmn = min(lmn, dg[k]);
+            }
+          }
+          const int incl = wave_scan_incl(lg);
+          xs_g = readlane(incl, WAVE - 1) - incl;
+          const int rmx = wave_scan_incl_max(__shfl(lmx, (WAVE - 1) - lane));
+          const int rmn = wave_scan_incl_min(__shfl(lmn, (WAVE - 1) - lane));
+          const int src = lane < WAVE - 1 ? (WAVE - 2) - lane : 0;
+          xs_max = __shfl(rmx, src);
+          xs_min = __shfl(rmn, src);
+          if (lane == WAVE - 1) {
+            xs_max = -1;
+            xs_min = IDLE;
           }
         }
+        // completion time of the first position of the next lane
+        const int e_up = t + (int)(uint32_t)__shfl_down((int)dk[0], 1);
+        // Stop position: the lowest position ending a tie group after which
+        // the machine is empty or A_max <= alpha (A_max right after the
+        // completions at e is e - t + the largest progress still active).
+        stop = quiet >= 3 ? quiet - 1 : N - 1;
+        if (POL == POL_ISJL && planned > 0) {
+          int cg_max = xs_max, lfound = IDLE;
+#pragma unroll
+          for (int k = KS - 1; k >= 0; --k) {
+            const int pos = lane * KS + k;
+            const bool valid = pos < N;
+            const int e = t + (int)dk[k];
+            const int e_next = (k + 1 < KS) ? t + (int)dk[k + 1 < KS ? k + 1 : k] : e_up;
+            const bool group_end = valid && (pos + 1 >= N || e_next > e);
+            if (group_end && (pos + 1 >= N || e - t + cg_max <= alpha)) lfound = pos;
+            if (valid) cg_max = max(cg_max, dg[k]);
+          }
+          stop = min(stop, wave_min(lfound));
+        }
+        // Spans between consecutive completions below `stop`, each with the
+        // jobs at the positions above (count N - 1 - p, progress suffix sums).
+        int sg = 0, sgmax = -1, sgmin = IDLE, se = 0;
+        {
+          int cg = xs_g, cg_max = xs_max, cg_min = xs_min;
+#pragma unroll
+          for (int k = KS - 1; k >= 0; --k) {
+            const int pos = lane * KS + k;
+            const bool valid = pos < N;
+            const int e = t + (int)dk[k];
+            const int e_next = (k + 1 < KS) ? t + (int)dk[k + 1 < KS ? k + 1 : k] : e_up;
+            if (valid && pos < stop && e_next > e) {
+              const int64_t D = (int64_t)(e_next - e);
+              const int64_t s = N - 1 - pos;
+              const int min_s = t - cg_max, max_s = t - cg_min;
+              const int64_t sum_s = s * (int64_t)t - cg;
+              const int64_t m0 = (int64_t)(e - min_s) + 1;
+              const int64_t sm = D * m0 + D * (D - 1) / 2;
+              lE += D * (sum_s - s * (int64_t)min_s);
+              lSM += sm;
+              lSSM += s * sm;
+              const int ext = max_s - min_s;
+              lX += D * ext;
+              if (ext > alpha) lU += (int)D;
+              lP = max(lP, s * (int64_t)e_next - sum_s);
+            }
+            if (pos == stop) {
+              sg = cg;
+              sgmax = cg_max;
+              sgmin = cg_min;
+              se = e;
+            }
+            if (valid) {
+              cg += dg[k];
+              cg_max = max(cg_max, dg[k]);
+              cg_min = min(cg_min, dg[k]);
+            }
+          }
+        }
+        const int Ls = stop / KS;
+        st_g = readlane(sg, Ls);
+        st_gmax = readlane(sgmax, Ls);
+        st_gmin = readlane(sgmin, Ls);
+        tau_end = readlane(se, Ls);
+        e0 = t + readlane((int)dk[0], 0);
+      };
+      if constexpr (K >= 4) {
+        if (packed && N <= WAVE) sweep_body(std::integral_constant<int, 1>{});
+        else sweep_body(std::integral_constant<int, K>{});
+      } else {
+        sweep_body(std::integral_constant<int, K>{});
       }
-      const int Ls = stop / K;
-      st_g = readlane(st_g, Ls);
-      st_gmax = readlane(st_gmax, Ls);
-      st_gmin = readlane(st_gmin, Ls);
-      const int tau_end = readlane(st_e, Ls);
       // span [t, e_0): every job still active; the set only shrinks after it,
       // so it also carries the largest extent and count of the sweep
       {
-        const int e0 = t + readlane((int)dk[0], 0);
         const int64_t D = (int64_t)(e0 - t), s = N;
         const int64_t m0 = (int64_t)(t - S.min_s) + 1;
         const int64_t sm = D * m0 + D * (D - 1) / 2;
