@@ -228,7 +228,7 @@ int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs
   a.c = p->cost_c;
   a.tau = p->cost_tau;
   a.NP2 = next_pow2(2 * n_jobs);
-  a.wave_words = a.NP2 + (n_jobs + 3) / 4;
+  a.wave_words = a.NP2 + n_jobs;  // sorted events, then the length of each job
   a.wave_words = (a.wave_words + 3) & ~3;
   const size_t per_wave = (size_t)a.wave_words * 4;
   int wpb = 4;

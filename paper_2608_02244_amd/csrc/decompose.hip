@@ -4,13 +4,10 @@
 // The 2n start/end events are sorted in LDS as packed keys
 //   time << 13 | kind << 12 | index      (kind 0 = end, 1 = start)
 // so that at equal times completions come before starts, matching the step
-// model (a job ending at t frees its slot for a job starting at t).  A sweep
-// over the sorted events keeps |S|, sum of starts and sum of reservations as
-// scalars; the earliest and latest start among the active jobs are found by
-// wave-parallel scans over the sorted events (forward from the previous
-// earliest, backward from the latest start event seen), 64 events per step.
-// Between two event times the active set is fixed and the Section 5 terms are
-// summed in closed form, as in the simulation kernel.
+// model (a job ending at t frees its slot for a job starting at t).  Between
+// two event times the active set is fixed and the Section 5 terms are summed
+// in closed form, as in the simulation kernel; the sweep itself is described
+// where it runs.
 #include "dec_common.hpp"
 #include "wave.hpp"
 
@@ -62,7 +59,7 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
   const int lane = lane_id();
   const int n = a.n;
   uint32_t* EV = lds_raw + (size_t)wib * (size_t)a.wave_words;
-  uint8_t* ST = (uint8_t*)(EV + a.NP2);  // per job: 0 not started, 1 active, 2 ended
+  int32_t* LEN = (int32_t*)(EV + a.NP2);  // per job: prompt + output
   const int64_t row = inst * (int64_t)n;
   const int32_t* A = a.arrival + row;
   const int32_t* P = a.prompt + row;
@@ -147,138 +144,197 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
     }
     EV[e] = key;
   }
-  for (int i = lane; i < n; i += WAVE) ST[i] = 0;
+  for (int i = lane; i < n; i += WAVE) LEN[i] = P[i] + O[i];
   wave_lds_sync();
   dec_sort(EV, NP2, lane);
 
   // ---- sweep ----------------------------------------------------------------
-  int cnt = 0, min_s = IDLE32, max_s = -1;
-  int pmin = 0;   // events before pmin hold no start of an active job
-  int pmax = -1;  // index of the latest start event processed
-  bool dirty_min = false, dirty_max = false;
-  int64_t sum_s = 0, res = 0;
-  int cur_t = 0;
-  uint32_t v = early ? 1u : 0u;
-  int64_t acc_E = 0, acc_C = 0, acc_W = 0, acc_ext = 0, acc_busy = 0, acc_peak = 0, acc_unf = 0;
-  int acc_maxext = 0, acc_maxact = 0;
+  // 64 sorted events at a time: |S|, the start sum and the reservation sum
+  // after each event are prefix scans of the events' deltas.  A group is the
+  // events of one time; the span after a group end lasts to the next event
+  // time.  The earliest / latest active start after a group end changes only
+  // when its holder ends (then it is searched again: forward from the earliest
+  // start event seen, backward from the latest, 64 events per step, a start
+  // event being active at time t when its job ends after t) or when the group
+  // starts jobs; that part walks the group ends of the chunk one by one, and
+  // the span terms are then summed for all group ends of the chunk at once.
   const int alpha = a.alpha;
   const int64_t M = a.M;
   const int Bcap = a.B;
+  uint32_t v = early ? 1u : 0u;
+  int c_cnt = 0;                       // |S| before the chunk
+  int64_t c_sum = 0, c_res = 0;        // start sum, reservation sum before the chunk
+  int min_s = IDLE32, max_s = -1;      // of the active set at the last group end
+  int pmin = 0, pmax = -1;             // positions of their start events
+  int cnt_prev = 0;                    // |S| at the last group end
+  bool dmin = false, dmax = false, gstart = false;  // pending for the open group
+  int gfirst = -1;                     // first start position of the open group
+  int64_t lE = 0, lC = 0, lW = 0, lX = 0, lB = 0, lU = 0, lP = 0;
+  int lXm = 0, lAm = 0;
+  bool lcap = false, lkv = false, lunf = false;
+  // idle steps before the first event
+  const int t_first = (int)(EV[0] >> 13);
+  const int64_t c0 = a.c * (int64_t)t_first;
 
   for (int base = 0; base < NE; base += WAVE) {
-    const int e = base + lane;
-    const uint32_t key = e < NE ? EV[e] : 0xFFFFFFFFu;
-    const int kt = (int)(key >> 13), kid = (int)(key & 0xFFFu);
-    const int klen = e < NE ? P[kid] + O[kid] : 0;
-    const int cnum = min(WAVE, NE - base);
-    for (int q = 0; q < cnum; ++q) {
-      const int t = readlane(kt, q);
-      if (t > cur_t) {
-        // refresh the earliest / latest active start if their holders ended
-        if (cnt > 0 && dirty_min) {
+    const int p = base + lane;
+    const bool valid = p < NE;
+    const uint32_t key = valid ? EV[p] : 0xFFFFFFFFu;
+    const int t = (int)(key >> 13);
+    const bool is_start = valid && ((key >> 12) & 1u);
+    const bool is_end = valid && !((key >> 12) & 1u);
+    const int len = valid ? LEN[key & 0xFFFu] : 0;
+    const int sj = is_start ? t : t - len;  // the job's start
+    const int cnt_p = c_cnt + wave_scan_incl(is_start ? 1 : (is_end ? -1 : 0));
+    const int64_t sum_p = c_sum + wave_scan_incl64(is_start ? (int64_t)sj : (is_end ? -(int64_t)sj : 0));
+    const int64_t res_p = c_res + wave_scan_incl64(is_start ? (int64_t)len : (is_end ? -(int64_t)len : 0));
+    int t_next = __shfl_down(t, 1);
+    if (lane == WAVE - 1) t_next = base + WAVE < NE ? (int)(EV[base + WAVE] >> 13) : t;
+    const bool last = p == NE - 1;
+    const bool gend = valid && (last || t_next > t);
+    uint64_t gm = ballot(gend);
+    const uint64_t m_start = ballot(is_start);
+    int gmin = IDLE32, gmax = -1;
+    int prevL = -1;
+    while (gm) {
+      const int gL = __builtin_ctzll(gm);
+      gm &= gm - 1;
+      const int tg = readlane(t, gL);
+      const uint64_t rmask = prevL < 0 ? (gL == 63 ? ~0ull : ((2ull << gL) - 1))
+                                       : ((gL == 63 ? ~0ull : ((2ull << gL) - 1)) & ~((2ull << prevL) - 1));
+      dmin = dmin || (ballot(is_end && sj == min_s) & rmask) != 0;
+      dmax = dmax || (ballot(is_end && sj == max_s) & rmask) != 0;
+      const uint64_t ms = m_start & rmask;
+      if (ms) {
+        if (!gstart) gfirst = base + __builtin_ctzll(ms);
+        gstart = true;
+      }
+      const int cnt_g = readlane(cnt_p, gL);
+      if (gstart) {
+        if (cnt_prev == 0) {
+          min_s = tg;
+          pmin = gfirst;
+          dmin = false;
+        }
+        max_s = tg;
+        if (ms) pmax = base + (63 - __builtin_clzll(ms));  // else set by the previous chunk
+        dmax = false;
+      }
+      if (cnt_g == 0) {
+        min_s = IDLE32;
+        max_s = -1;
+        dmin = dmax = false;
+      } else {
+        if (dmin) {
           while (true) {
-            int ee = pmin + lane;
+            const int ee = pmin + lane;
             bool hit = false;
             int st_time = 0;
-            if (ee < NE) {
-              uint32_t kk = EV[ee];
-              hit = ((kk >> 12) & 1u) && ST[kk & 0xFFFu] == 1;
+            if (ee < NE && ee <= base + gL) {
+              const uint32_t kk = EV[ee];
               st_time = (int)(kk >> 13);
+              hit = ((kk >> 12) & 1u) && st_time + LEN[kk & 0xFFFu] > tg;
             }
-            uint64_t m = ballot(hit);
-            if (m) {
-              int L = __builtin_ctzll(m);
+            const uint64_t hm = ballot(hit);
+            if (hm) {
+              const int L = __builtin_ctzll(hm);
               pmin += L;
               min_s = readlane(st_time, L);
               break;
             }
             pmin += WAVE;
-            if (pmin >= NE) break;  // unreachable while cnt > 0
+            if (pmin > base + gL) break;  // unreachable while |S| > 0
           }
-          dirty_min = false;
+          dmin = false;
         }
-        if (cnt > 0 && dirty_max) {
+        if (dmax) {
           while (true) {
-            int ee = pmax - lane;
+            const int ee = pmax - lane;
             bool hit = false;
             int st_time = 0;
             if (ee >= 0) {
-              uint32_t kk = EV[ee];
-              hit = ((kk >> 12) & 1u) && ST[kk & 0xFFFu] == 1;
+              const uint32_t kk = EV[ee];
               st_time = (int)(kk >> 13);
+              hit = ((kk >> 12) & 1u) && st_time + LEN[kk & 0xFFFu] > tg;
             }
-            uint64_t m = ballot(hit);
-            if (m) {
-              int L = __builtin_ctzll(m);
+            const uint64_t hm = ballot(hit);
+            if (hm) {
+              const int L = __builtin_ctzll(hm);
               pmax -= L;
               max_s = readlane(st_time, L);
               break;
             }
             pmax -= WAVE;
-            if (pmax < 0) break;  // unreachable while cnt > 0
+            if (pmax < 0) break;  // unreachable while |S| > 0
           }
-          dirty_max = false;
-        }
-        // account steps cur_t .. t-1 (Section 5)
-        const int64_t D = (int64_t)(t - cur_t);
-        if (cnt == 0) {
-          acc_C += a.c * D;
-          acc_W += a.c * D;
-        } else {
-          const int64_t s = cnt;
-          const int64_t m0 = (int64_t)(cur_t - min_s) + 1;
-          const int64_t sm = D * m0 + D * (D - 1) / 2;
-          acc_E += D * (sum_s - s * (int64_t)min_s);
-          acc_C += a.c * D + a.tau * s * sm;
-          acc_W += a.c * D + a.tau * sm;
-          const int ext = max_s - min_s;
-          acc_ext += D * ext;
-          acc_busy += D;
-          if (ext > alpha) {
-            acc_unf += D;
-            v |= 8u;
-          }
-          acc_maxext = max(acc_maxext, ext);
-          acc_maxact = max(acc_maxact, cnt);
-          acc_peak = max(acc_peak, s * (int64_t)t - sum_s);
-          if (Bcap > 0 && cnt > Bcap) v |= 2u;
-          if (M != 0 && cnt >= 2 && res > M) v |= 4u;
-        }
-        cur_t = t;
-      }
-      const uint32_t kq = (uint32_t)readlane((int)key, q);
-      const int id = (int)(kq & 0xFFFu);
-      const int len = readlane(klen, q);
-      if ((kq >> 12) & 1u) {  // start
-        if (cnt == 0) {
-          min_s = t;
-          pmin = base + q;
-          dirty_min = false;
-        }
-        cnt++;
-        sum_s += t;
-        res += len;
-        max_s = t;
-        pmax = base + q;
-        dirty_max = false;
-        if (lane == 0) ST[id] = 1;
-      } else {  // end
-        const int s = t - len;
-        cnt--;
-        sum_s -= s;
-        res -= len;
-        if (lane == 0) ST[id] = 2;
-        if (s == min_s) dirty_min = true;
-        if (s == max_s) dirty_max = true;
-        if (cnt == 0) {
-          min_s = IDLE32;
-          max_s = -1;
-          dirty_min = dirty_max = false;
+          dmax = false;
         }
       }
-      wave_lds_sync();
+      if (lane == gL) {
+        gmin = min_s;
+        gmax = max_s;
+      }
+      cnt_prev = cnt_g;
+      gstart = false;
+      prevL = gL;
     }
+    // events after the chunk's last group end belong to the next group
+    {
+      const uint64_t rmask = prevL < 0 ? ~0ull : (prevL == 63 ? 0ull : ~((2ull << prevL) - 1));
+      dmin = dmin || (ballot(is_end && sj == min_s) & rmask) != 0;
+      dmax = dmax || (ballot(is_end && sj == max_s) & rmask) != 0;
+      const uint64_t ms = m_start & rmask;
+      if (ms) {
+        if (!gstart) gfirst = base + __builtin_ctzll(ms);
+        gstart = true;
+        // the open group's latest start so far
+        pmax = base + (63 - __builtin_clzll(ms));
+      }
+    }
+    // span terms of every group end of the chunk (the span runs to the next
+    // event time; the last event has none)
+    if (gend && !last && t_next > t) {
+      const int64_t D = (int64_t)(t_next - t);
+      if (cnt_p == 0) {
+        lC += a.c * D;
+        lW += a.c * D;
+      } else {
+        const int64_t s = cnt_p;
+        const int64_t m0 = (int64_t)(t - gmin) + 1;
+        const int64_t sm = D * m0 + D * (D - 1) / 2;
+        lE += D * (sum_p - s * (int64_t)gmin);
+        lC += a.c * D + a.tau * s * sm;
+        lW += a.c * D + a.tau * sm;
+        const int ext = gmax - gmin;
+        lX += D * ext;
+        lB += D;
+        if (ext > alpha) {
+          lU += D;
+          lunf = true;
+        }
+        lXm = max(lXm, ext);
+        lAm = max(lAm, cnt_p);
+        lP = max(lP, s * (int64_t)t_next - sum_p);
+        if (Bcap > 0 && cnt_p > Bcap) lcap = true;
+        if (M != 0 && cnt_p >= 2 && res_p > M) lkv = true;
+      }
+    }
+    c_cnt = readlane(cnt_p, 63);
+    c_sum = readlane64(sum_p, 63);
+    c_res = readlane64(res_p, 63);
   }
+  const int64_t acc_E = wave_sum64(lE);
+  const int64_t acc_C = c0 + wave_sum64(lC);
+  const int64_t acc_W = c0 + wave_sum64(lW);
+  const int64_t acc_ext = wave_sum64(lX);
+  const int64_t acc_busy = wave_sum64(lB);
+  const int64_t acc_unf = wave_sum64(lU);
+  const int64_t acc_peak = wave_max64(lP);
+  const int acc_maxext = wave_max(lXm);
+  const int acc_maxact = wave_max(lAm);
+  if (ballot(lunf)) v |= 8u;
+  if (ballot(lcap)) v |= 2u;
+  if (ballot(lkv)) v |= 4u;
 
   if (lane == 0) {
     fsched_metrics m;

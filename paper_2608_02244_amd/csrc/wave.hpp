@@ -150,12 +150,28 @@ __device__ __forceinline__ int shfl_xor_c(int v) {
 }
 
 // DPP move of a 64-bit value (both halves with the same control word).
-template <int CTRL, int ROW_MASK = 0xf, int BANK_MASK = 0xf>
+template <int CTRL, int ROW_MASK = 0xf, int BANK_MASK = 0xf, bool BOUND = false>
 __device__ __forceinline__ uint64_t dpp64(uint64_t old, uint64_t src) {
-  const uint32_t lo = (uint32_t)dpp<CTRL, ROW_MASK, BANK_MASK>((int)(uint32_t)old, (int)(uint32_t)src);
-  const uint32_t hi = (uint32_t)dpp<CTRL, ROW_MASK, BANK_MASK>((int)(uint32_t)(old >> 32),
-                                                               (int)(uint32_t)(src >> 32));
+  const uint32_t lo =
+      (uint32_t)dpp<CTRL, ROW_MASK, BANK_MASK, BOUND>((int)(uint32_t)old, (int)(uint32_t)src);
+  const uint32_t hi = (uint32_t)dpp<CTRL, ROW_MASK, BANK_MASK, BOUND>(
+      (int)(uint32_t)(old >> 32), (int)(uint32_t)(src >> 32));
   return ((uint64_t)hi << 32) | lo;
+}
+
+// Inclusive prefix sum of 64-bit values over lanes 0..63 (same DPP pattern as
+// the 32-bit scan).
+__device__ __forceinline__ int64_t wave_scan_incl64(int64_t x) {
+  const uint64_t s = (uint64_t)x;
+  uint64_t v = s;
+  v += dpp64<DPP_ROW_SHR1, 0xf, 0xf, true>(0, s);
+  v += dpp64<DPP_ROW_SHR2, 0xf, 0xf, true>(0, s);
+  v += dpp64<DPP_ROW_SHR3, 0xf, 0xf, true>(0, s);
+  v += dpp64<DPP_ROW_SHR4, 0xf, 0xe>(0, v);
+  v += dpp64<DPP_ROW_SHR8, 0xf, 0xc>(0, v);
+  v += dpp64<DPP_BCAST15, 0xa, 0xf>(0, v);
+  v += dpp64<DPP_BCAST31, 0xc, 0xf>(0, v);
+  return (int64_t)v;
 }
 
 __device__ __forceinline__ int64_t readlane64(int64_t v, int l) {
