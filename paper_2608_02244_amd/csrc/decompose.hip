@@ -153,28 +153,53 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
   // after each event are prefix scans of the events' deltas.  A group is the
   // events of one time; the span after a group end lasts to the next event
   // time.  The earliest / latest active start after a group end changes only
-  // when its holder ends (then it is searched again: forward from the earliest
-  // start event seen, backward from the latest, 64 events per step, a start
-  // event being active at time t when its job ends after t) or when the group
-  // starts jobs; that part walks the group ends of the chunk one by one, and
-  // the span terms are then summed for all group ends of the chunk at once.
+  // when the group starts jobs or when the last active job holding it ends, so
+  // only those group ends are visited one by one: the earliest start is kept
+  // with the number of active jobs that started then (nmin; the same for the
+  // latest, nmax), and a group end is visited when it has starts or when the
+  // ends since the last visit use up nmin or nmax.  A start event is active at
+  // time t when its job ends after t; a new earliest (latest) start is searched
+  // forward (backward) from the previous one, 64 events per step.  The values
+  // in force at every group end are then spread by lane and the span terms of
+  // all group ends of the chunk are summed at once.
   const int alpha = a.alpha;
   const int64_t M = a.M;
   const int Bcap = a.B;
   uint32_t v = early ? 1u : 0u;
   int c_cnt = 0;                       // |S| before the chunk
   int64_t c_sum = 0, c_res = 0;        // start sum, reservation sum before the chunk
-  int min_s = IDLE32, max_s = -1;      // of the active set at the last group end
-  int pmin = 0, pmax = -1;             // positions of their start events
-  int cnt_prev = 0;                    // |S| at the last group end
-  bool dmin = false, dmax = false, gstart = false;  // pending for the open group
-  int gfirst = -1;                     // first start position of the open group
+  int min_s = IDLE32, max_s = -1;      // earliest / latest active start
+  int nmin = 0, nmax = 0;              // active jobs that started at min_s / max_s
+  int pmin = 0, pmax = -1;             // first / last of their start events
+  int cnt_last = 0;                    // |S| at the last group end
+  int g_nst = 0, gfirst = -1, glast = -1;  // starts of the open group (before this chunk)
   int64_t lE = 0, lC = 0, lW = 0, lX = 0, lB = 0, lU = 0, lP = 0;
   int lXm = 0, lAm = 0;
   bool lcap = false, lkv = false, lunf = false;
   // idle steps before the first event
   const int t_first = (int)(EV[0] >> 13);
   const int64_t c0 = a.c * (int64_t)t_first;
+
+  // position of the k-th set bit (k >= 1) of m, which has at least k
+  auto kth_bit = [](uint64_t m, int k) -> int {
+    int pos = 0;
+#pragma unroll
+    for (int w = 32; w >= 1; w >>= 1) {
+      const uint64_t low = m & ((1ull << w) - 1);
+      const int c = __builtin_popcountll(low);
+      if (k > c) {
+        k -= c;
+        m >>= w;
+        pos += w;
+      } else {
+        m = low;
+      }
+    }
+    return pos;
+  };
+  auto bits_above = [](int d) -> uint64_t {  // lanes > d (d in -1 .. 63)
+    return d < 0 ? ~0ull : (d >= 63 ? 0ull : ~((2ull << d) - 1));
+  };
 
   for (int base = 0; base < NE; base += WAVE) {
     const int p = base + lane;
@@ -186,114 +211,179 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
     const int len = valid ? LEN[key & 0xFFFu] : 0;
     const int sj = is_start ? t : t - len;  // the job's start
     const int cnt_p = c_cnt + wave_scan_incl(is_start ? 1 : (is_end ? -1 : 0));
-    const int64_t sum_p = c_sum + wave_scan_incl64(is_start ? (int64_t)sj : (is_end ? -(int64_t)sj : 0));
-    const int64_t res_p = c_res + wave_scan_incl64(is_start ? (int64_t)len : (is_end ? -(int64_t)len : 0));
+    const int64_t sum_p =
+        c_sum + wave_scan_incl64(is_start ? (int64_t)sj : (is_end ? -(int64_t)sj : 0));
+    const int64_t res_p =
+        c_res + wave_scan_incl64(is_start ? (int64_t)len : (is_end ? -(int64_t)len : 0));
     int t_next = __shfl_down(t, 1);
     if (lane == WAVE - 1) t_next = base + WAVE < NE ? (int)(EV[base + WAVE] >> 13) : t;
     const bool last = p == NE - 1;
     const bool gend = valid && (last || t_next > t);
-    uint64_t gm = ballot(gend);
-    const uint64_t m_start = ballot(is_start);
-    int gmin = IDLE32, gmax = -1;
-    int prevL = -1;
-    while (gm) {
-      const int gL = __builtin_ctzll(gm);
-      gm &= gm - 1;
-      const int tg = readlane(t, gL);
-      const uint64_t rmask = prevL < 0 ? (gL == 63 ? ~0ull : ((2ull << gL) - 1))
-                                       : ((gL == 63 ? ~0ull : ((2ull << gL) - 1)) & ~((2ull << prevL) - 1));
-      dmin = dmin || (ballot(is_end && sj == min_s) & rmask) != 0;
-      dmax = dmax || (ballot(is_end && sj == max_s) & rmask) != 0;
-      const uint64_t ms = m_start & rmask;
-      if (ms) {
-        if (!gstart) gfirst = base + __builtin_ctzll(ms);
-        gstart = true;
+    const uint64_t gmask = ballot(gend);
+    const uint64_t smask = ballot(is_start);
+    uint64_t emin = ballot(is_end && sj == min_s);
+    uint64_t emax = ballot(is_end && sj == max_s);
+    const int min0 = min_s, max0 = max_s;  // in force before the chunk's first visit
+    uint64_t chg = 0;                      // visited group ends
+    int vmin = 0, vmax = 0;                // values set there
+    int done = -1;                         // lanes <= done are accounted for
+    bool open = g_nst > 0;                 // the first group of the chunk began earlier
+    while (true) {
+      const uint64_t after = bits_above(done);
+      const uint64_t ge = gmask & after;
+      if (!ge) break;
+      // the earliest position after `done` at which something can change
+      int x = WAVE;
+      if (open || (min_s != IDLE32 && nmin <= 0) || (max_s >= 0 && nmax <= 0)) x = 0;
+      const uint64_t sa = smask & after;
+      if (sa) x = min(x, __builtin_ctzll(sa));
+      if (min_s != IDLE32) {
+        const uint64_t ea = emin & after;
+        if (__builtin_popcountll(ea) >= nmin && nmin > 0) x = min(x, kth_bit(ea, nmin));
       }
+      if (max_s >= 0) {
+        const uint64_t ea = emax & after;
+        if (__builtin_popcountll(ea) >= nmax && nmax > 0) x = min(x, kth_bit(ea, nmax));
+      }
+      if (x == WAVE) break;
+      const uint64_t gx = ge & ~((1ull << x) - 1);
+      if (!gx) break;  // the group ends in the next chunk
+      const int gL = __builtin_ctzll(gx);
+      const uint64_t rng = after & (gL == 63 ? ~0ull : ((2ull << gL) - 1));
+      const int tg = readlane(t, gL);
       const int cnt_g = readlane(cnt_p, gL);
-      if (gstart) {
-        if (cnt_prev == 0) {
+      // |S| before this group: at the previous group end
+      const uint64_t gprev = gmask & ((1ull << gL) - 1);
+      const int cnt_before = gprev ? readlane(cnt_p, 63 - __builtin_clzll(gprev)) : cnt_last;
+      nmin -= __builtin_popcountll(emin & rng);
+      nmax -= __builtin_popcountll(emax & rng);
+      const uint64_t sr = smask & rng;
+      const bool with_open = open && !gprev;
+      const int nst = __builtin_popcountll(sr) + (with_open ? g_nst : 0);
+      if (nst > 0) {
+        const int gf = with_open ? gfirst : base + __builtin_ctzll(sr);
+        const int gl = sr ? base + 63 - __builtin_clzll(sr) : glast;
+        if (cnt_before == 0) {
           min_s = tg;
-          pmin = gfirst;
-          dmin = false;
+          nmin = nst;
+          pmin = gf;
         }
         max_s = tg;
-        if (ms) pmax = base + (63 - __builtin_clzll(ms));  // else set by the previous chunk
-        dmax = false;
+        nmax = nst;
+        pmax = gl;
       }
+      open = open && gprev;  // a group end before gL closed the open group
+      if (with_open) open = false;
+      const int gpos = base + gL;
       if (cnt_g == 0) {
         min_s = IDLE32;
         max_s = -1;
-        dmin = dmax = false;
+        nmin = nmax = 0;
       } else {
-        if (dmin) {
-          while (true) {
-            const int ee = pmin + lane;
-            bool hit = false;
+        if (nmin <= 0) {
+          // first active start event at or after pmin; then count the active
+          // ones at that time
+          int q = max(pmin, 0), found = -1, cnt = 0;
+          while (q <= gpos) {
+            const int ee = q + lane;
+            bool ok = false;
             int st_time = 0;
-            if (ee < NE && ee <= base + gL) {
+            if (ee >= 0 && ee <= gpos) {
               const uint32_t kk = EV[ee];
               st_time = (int)(kk >> 13);
-              hit = ((kk >> 12) & 1u) && st_time + LEN[kk & 0xFFFu] > tg;
+              ok = ((kk >> 12) & 1u) && st_time + LEN[kk & 0xFFFu] > tg;
             }
-            const uint64_t hm = ballot(hit);
-            if (hm) {
-              const int L = __builtin_ctzll(hm);
-              pmin += L;
-              min_s = readlane(st_time, L);
-              break;
+            if (found < 0) {
+              const uint64_t hm = ballot(ok);
+              if (hm) {
+                const int L = __builtin_ctzll(hm);
+                found = q + L;
+                min_s = readlane(st_time, L);
+              }
             }
-            pmin += WAVE;
-            if (pmin > base + gL) break;  // unreachable while |S| > 0
+            if (found >= 0) {
+              cnt += __builtin_popcountll(ballot(ok && st_time == min_s));
+              if (ballot(ee >= 0 && ee <= gpos && st_time > min_s)) break;
+            }
+            q += WAVE;
           }
-          dmin = false;
+          pmin = found;
+          nmin = cnt;
         }
-        if (dmax) {
-          while (true) {
-            const int ee = pmax - lane;
-            bool hit = false;
+        if (nmax <= 0) {
+          // last active start event at or before pmax; then count the active
+          // ones at that time
+          int q = pmax, found = -1, cnt = 0;
+          while (q >= 0) {
+            const int ee = q - lane;
+            bool ok = false;
             int st_time = 0;
             if (ee >= 0) {
               const uint32_t kk = EV[ee];
               st_time = (int)(kk >> 13);
-              hit = ((kk >> 12) & 1u) && st_time + LEN[kk & 0xFFFu] > tg;
+              ok = ((kk >> 12) & 1u) && st_time + LEN[kk & 0xFFFu] > tg;
             }
-            const uint64_t hm = ballot(hit);
-            if (hm) {
-              const int L = __builtin_ctzll(hm);
-              pmax -= L;
-              max_s = readlane(st_time, L);
-              break;
+            if (found < 0) {
+              const uint64_t hm = ballot(ok);
+              if (hm) {
+                const int L = __builtin_ctzll(hm);
+                found = q - L;
+                max_s = readlane(st_time, L);
+              }
             }
-            pmax -= WAVE;
-            if (pmax < 0) break;  // unreachable while |S| > 0
+            if (found >= 0) {
+              cnt += __builtin_popcountll(ballot(ok && st_time == max_s));
+              if (ballot(ee >= 0 && st_time < max_s)) break;
+            }
+            q -= WAVE;
           }
-          dmax = false;
+          pmax = found;
+          nmax = cnt;
         }
       }
+      chg |= 1ull << gL;
       if (lane == gL) {
-        gmin = min_s;
-        gmax = max_s;
+        vmin = min_s;
+        vmax = max_s;
       }
-      cnt_prev = cnt_g;
-      gstart = false;
-      prevL = gL;
+      emin = ballot(is_end && sj == min_s);
+      emax = ballot(is_end && sj == max_s);
+      done = gL;
     }
-    // events after the chunk's last group end belong to the next group
+    // the rest of the chunk: groups with nothing to change, then the open group
     {
-      const uint64_t rmask = prevL < 0 ? ~0ull : (prevL == 63 ? 0ull : ~((2ull << prevL) - 1));
-      dmin = dmin || (ballot(is_end && sj == min_s) & rmask) != 0;
-      dmax = dmax || (ballot(is_end && sj == max_s) & rmask) != 0;
-      const uint64_t ms = m_start & rmask;
-      if (ms) {
-        if (!gstart) gfirst = base + __builtin_ctzll(ms);
-        gstart = true;
-        // the open group's latest start so far
-        pmax = base + (63 - __builtin_clzll(ms));
+      const uint64_t after = bits_above(done);
+      nmin -= __builtin_popcountll(emin & after);
+      nmax -= __builtin_popcountll(emax & after);
+      const uint64_t glast_m = gmask & after;
+      if (glast_m) open = false;
+      const uint64_t tail = bits_above(gmask ? 63 - __builtin_clzll(gmask) : -1) & after;
+      const uint64_t st = smask & tail;
+      if (st) {
+        if (!open) {
+          g_nst = 0;
+          gfirst = base + __builtin_ctzll(st);
+        }
+        g_nst += __builtin_popcountll(st);
+        glast = base + 63 - __builtin_clzll(st);
+        open = true;
       }
+      if (!open) g_nst = 0;
+      if (gmask) cnt_last = readlane(cnt_p, 63 - __builtin_clzll(gmask));
+    }
+    // earliest / latest start in force at each group end of the chunk
+    int gmin, gmax;
+    {
+      const uint64_t upto = lane == 63 ? ~0ull : ((2ull << lane) - 1);
+      const uint64_t c = chg & upto;
+      const int src = c ? 63 - __builtin_clzll(c) : 0;
+      const int fmin = __shfl(vmin, src), fmax = __shfl(vmax, src);
+      gmin = c ? fmin : min0;
+      gmax = c ? fmax : max0;
     }
     // span terms of every group end of the chunk (the span runs to the next
     // event time; the last event has none)
-    if (gend && !last && t_next > t) {
+    if (gend && !last) {
       const int64_t D = (int64_t)(t_next - t);
       if (cnt_p == 0) {
         lC += a.c * D;

@@ -94,6 +94,26 @@ def test_random_start_vectors(dev):
     assert True
 
 
+def test_random_start_vectors_large(dev):
+    """Large instances: event groups that span several 64-event chunks, long and
+    short jobs mixed, every kind of budget."""
+    rng = np.random.default_rng(1234)
+    for trial in range(12):
+        n = int(rng.choice([500, 1000, 2048, 4096]))
+        a, p, o = workload.random_tables(rng, 6, n, 8, int(rng.choice([3, 40, 900])),
+                                         max_arrival=int(rng.choice([0, 100])))
+        span = int(rng.choice([2, 10, 300, 5000]))
+        s = (a + rng.integers(0, span, size=a.shape)).astype(np.int32)
+        kw = dict(B=int(rng.choice([0, 16, 300])), alpha=int(rng.choice([0, 5, 200, ALPHA_INF])),
+                  M_kv=int(rng.choice([0, 500, 20000])), cost_c=int(rng.integers(0, 50)),
+                  cost_tau=int(rng.integers(0, 5)))
+        ctx = f"large random starts trial={trial} n={n} span={span} {kw}"
+        log(ctx)
+        ref, rv = oracle.decompose(a, p, o, s, **kw)
+        got, gv = gpu_dec(dev, a, p, o, s, **kw)
+        same(ctx, got, ref, gv, rv)
+
+
 def test_limits_and_host_mode(dev):
     a = np.zeros((2, 3), np.int32)
     p = np.zeros((2, 3), np.int32)
