@@ -26,7 +26,8 @@ UNIT = "instance-steps/s"
 # gfx950: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = int32 VALU lane operations per second
 PEAK_ALU = 256 * 64 * 2.4e9
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "simulate_isjl_pareto_65536x2000_hbm.md")
-KERNEL_SOURCES = ["sim_kernel.hpp", "sim_common.hpp", "wave.hpp", "sim_isjl.hip", "abi.cpp"]
+KERNEL_SOURCES = ["sim_kernel.hpp", "sim_common.hpp", "regsort.hpp", "wave.hpp", "sim_isjl.hip",
+                  "abi.cpp"]
 
 
 def kernel_sources_sha256() -> str:

@@ -1,7 +1,8 @@
 // Re-scoring of given schedules (Section 5, Theorem 5.1; eq. (1) checks):
 // one wavefront per instance.
 //
-// The 2n start/end events are sorted in LDS as packed keys
+// The 2n start/end events are sorted (in registers, or in LDS beyond 4,096
+// events) as packed keys
 //   time << 13 | kind << 12 | index      (kind 0 = end, 1 = start)
 // so that at equal times completions come before starts, matching the step
 // model (a job ending at t frees its slot for a job starting at t).  Between
@@ -9,6 +10,7 @@
 // in closed form, as in the simulation kernel; the sweep itself is described
 // where it runs.
 #include "dec_common.hpp"
+#include "regsort.hpp"
 #include "wave.hpp"
 
 namespace fs {
@@ -146,7 +148,17 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
   }
   for (int i = lane; i < n; i += WAVE) LEN[i] = P[i] + O[i];
   wave_lds_sync();
-  dec_sort(EV, NP2, lane);
+  switch (NP2) {  // register sort up to 64 keys per lane, LDS network beyond
+    case 64: wave_reg_sort<1>(EV, lane); break;
+    case 128: wave_reg_sort<2>(EV, lane); break;
+    case 256: wave_reg_sort<4>(EV, lane); break;
+    case 512: wave_reg_sort<8>(EV, lane); break;
+    case 1024: wave_reg_sort<16>(EV, lane); break;
+    case 2048: wave_reg_sort<32>(EV, lane); break;
+    case 4096: wave_reg_sort<64>(EV, lane); break;
+    default: dec_sort(EV, NP2, lane); break;
+  }
+  wave_lds_sync();
 
   // ---- sweep ----------------------------------------------------------------
   // 64 sorted events at a time: |S|, the start sum and the reservation sum

@@ -1,0 +1,201 @@
+// Register bitonic sorts of one wavefront's keys (64 * KS of them, KS per
+// lane), used for the priority order, the drain sweep and the event order of
+// the re-scoring kernel.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "wave.hpp"
+
+namespace fs {
+
+// Lane-major register sort of 64 * KS keys: position p = lane * KS + k, so
+// the exchanges of distance below KS stay inside a lane and only the longer
+// ones cross lanes.  Ascending, keys only, in the form of the bitonic network
+// whose comparators all point the same way: each merge of two sorted blocks of
+// size/2 first compares p with its mirror p ^ (size - 1), then half-cleans
+// with p ^ d for d = size/4 .. 1; the lower position keeps the minimum.
+template <int M>
+__device__ __forceinline__ int shfl_mirror_c(int v) {
+  // value of lane (lane ^ M), M = 2^j - 1
+  if constexpr (M == 1) return dpp<DPP_QP_XOR1>(v, v);
+  else if constexpr (M == 3) return dpp<0x1B>(v, v);  // quad_perm [3,2,1,0]
+  else if constexpr (M == 7) return dpp<DPP_HALF_MIRROR>(v, v);
+  else if constexpr (M == 15) return dpp<DPP_MIRROR>(v, v);
+  else if constexpr (M == 31) return __builtin_amdgcn_ds_swizzle(v, (31 << 10) | 0x1F);
+  else return __shfl_xor(v, 63);
+}
+
+template <int SZ, int KS>  // mirror inside a lane's registers (block of SZ <= KS)
+__device__ __forceinline__ void lm_mirror_regs(uint32_t (&key)[KS]) {
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    if ((k & (SZ >> 1)) == 0) {
+      const int h = k ^ (SZ - 1);
+      const uint32_t x = key[k], y = key[h];
+      key[k] = min(x, y);
+      key[h] = max(x, y);
+    }
+  }
+}
+
+template <int M, int KS>  // mirror across lanes: lane ^ M, register KS - 1 - k
+__device__ __forceinline__ void lm_mirror_lanes(uint32_t (&key)[KS], int lane) {
+  const bool lower = (lane & ((M + 1) >> 1)) == 0;
+#pragma unroll
+  for (int k = 0; k < KS / 2 + (KS & 1); ++k) {
+    const int h = KS - 1 - k;
+    const uint32_t a = key[k], b = key[h];
+    const uint32_t pa = (uint32_t)shfl_mirror_c<M>((int)b);
+    if (h != k) {
+      const uint32_t pb = (uint32_t)shfl_mirror_c<M>((int)a);
+      key[h] = lower ? min(b, pb) : max(b, pb);
+    }
+    key[k] = lower ? min(a, pa) : max(a, pa);
+  }
+}
+
+template <int DK, int KS>  // half-cleaner inside a lane: registers k and k | DK
+__device__ __forceinline__ void lm_half_regs(uint32_t (&key)[KS]) {
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    if ((k & DK) == 0) {
+      const uint32_t x = key[k], y = key[k | DK];
+      key[k] = min(x, y);
+      key[k | DK] = max(x, y);
+    }
+  }
+}
+
+template <int D, int KS>  // half-cleaner across lanes: lane ^ D, same register
+__device__ __forceinline__ void lm_half_lanes(uint32_t (&key)[KS], int lane) {
+  const bool lower = (lane & D) == 0;
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    const uint32_t pk = (uint32_t)shfl_xor_c<D>((int)key[k]);
+    key[k] = lower ? min(key[k], pk) : max(key[k], pk);
+  }
+}
+
+// Sort the 64 * KS keys held in registers, ascending in lane-major order.
+template <int KS>
+__device__ inline void reg_sort_keys(uint32_t (&key)[KS], int lane) {
+  for (int size = 2; size <= KS * WAVE; size <<= 1) {
+    if (size <= KS) {
+      switch (size) {
+        case 2: if constexpr (KS >= 2) lm_mirror_regs<2>(key); break;
+        case 4: if constexpr (KS >= 4) lm_mirror_regs<4>(key); break;
+        case 8: if constexpr (KS >= 8) lm_mirror_regs<8>(key); break;
+        case 16: if constexpr (KS >= 16) lm_mirror_regs<16>(key); break;
+        case 32: if constexpr (KS >= 32) lm_mirror_regs<32>(key); break;
+        default: if constexpr (KS >= 64) lm_mirror_regs<64>(key); break;
+      }
+    } else {
+      switch (size / KS) {
+        case 2: lm_mirror_lanes<1>(key, lane); break;
+        case 4: lm_mirror_lanes<3>(key, lane); break;
+        case 8: lm_mirror_lanes<7>(key, lane); break;
+        case 16: lm_mirror_lanes<15>(key, lane); break;
+        case 32: lm_mirror_lanes<31>(key, lane); break;
+        default: lm_mirror_lanes<63>(key, lane); break;
+      }
+    }
+    for (int d = size >> 2; d > 0; d >>= 1) {
+      if (d < KS) {
+        switch (d) {
+          case 1: if constexpr (KS > 1) lm_half_regs<1>(key); break;
+          case 2: if constexpr (KS > 2) lm_half_regs<2>(key); break;
+          case 4: if constexpr (KS > 4) lm_half_regs<4>(key); break;
+          case 8: if constexpr (KS > 8) lm_half_regs<8>(key); break;
+          case 16: if constexpr (KS > 16) lm_half_regs<16>(key); break;
+          default: if constexpr (KS > 32) lm_half_regs<32>(key); break;
+        }
+      } else {
+        switch (d / KS) {
+          case 1: lm_half_lanes<1>(key, lane); break;
+          case 2: lm_half_lanes<2>(key, lane); break;
+          case 4: lm_half_lanes<4>(key, lane); break;
+          case 8: lm_half_lanes<8>(key, lane); break;
+          case 16: lm_half_lanes<16>(key, lane); break;
+          default: lm_half_lanes<32>(key, lane); break;
+        }
+      }
+    }
+  }
+}
+
+// The same network with one payload word per key (equal keys keep their own
+// payloads, a valid outcome of an exchange).
+template <int DK, int KS>
+__device__ __forceinline__ void lmp_cx_regs(uint32_t (&key)[KS], int (&val)[KS], int size,
+                                            int lane) {
+  const bool lane_asc = ((lane * KS) & size) == 0;
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    if ((k & DK) == 0) {
+      const int h = k | DK;
+      const bool asc = lane_asc && (k & size) == 0;
+      const uint32_t x = key[k], y = key[h];
+      const int vx = val[k], vy = val[h];
+      const bool sw = asc ? (x > y) : (x < y);
+      key[k] = sw ? y : x;
+      key[h] = sw ? x : y;
+      val[k] = sw ? vy : vx;
+      val[h] = sw ? vx : vy;
+    }
+  }
+}
+
+template <int D, int KS>
+__device__ __forceinline__ void lmp_cx_lanes(uint32_t (&key)[KS], int (&val)[KS], int size,
+                                             int lane) {
+  const bool take_min = ((lane & D) == 0) == (((lane * KS) & size) == 0);
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    const uint32_t pk = (uint32_t)shfl_xor_c<D>((int)key[k]);
+    const int pv = shfl_xor_c<D>(val[k]);
+    const uint32_t nk = take_min ? min(key[k], pk) : max(key[k], pk);
+    val[k] = nk == key[k] ? val[k] : pv;
+    key[k] = nk;
+  }
+}
+
+template <int KS>
+__device__ inline void reg_sort_payload(uint32_t (&key)[KS], int (&val)[KS], int lane) {
+  for (int size = 2; size <= KS * WAVE; size <<= 1) {
+    for (int d = size >> 1; d > 0; d >>= 1) {
+      if (d < KS) {
+        switch (d) {
+          case 1: if constexpr (KS > 1) lmp_cx_regs<1>(key, val, size, lane); break;
+          case 2: if constexpr (KS > 2) lmp_cx_regs<2>(key, val, size, lane); break;
+          case 4: if constexpr (KS > 4) lmp_cx_regs<4>(key, val, size, lane); break;
+          default: if constexpr (KS > 8) lmp_cx_regs<8>(key, val, size, lane); break;
+        }
+      } else {
+        switch (d / KS) {
+          case 1: lmp_cx_lanes<1>(key, val, size, lane); break;
+          case 2: lmp_cx_lanes<2>(key, val, size, lane); break;
+          case 4: lmp_cx_lanes<4>(key, val, size, lane); break;
+          case 8: lmp_cx_lanes<8>(key, val, size, lane); break;
+          case 16: lmp_cx_lanes<16>(key, val, size, lane); break;
+          default: lmp_cx_lanes<32>(key, val, size, lane); break;
+        }
+      }
+    }
+  }
+}
+
+// Sort W[0 .. 64*KS) ascending through registers (W is read in any order and
+// written back sorted).
+template <int KS>
+__device__ inline void wave_reg_sort(uint32_t* W, int lane) {
+  uint32_t key[KS];
+#pragma unroll
+  for (int k = 0; k < KS; ++k) key[k] = W[k * WAVE + lane];
+  reg_sort_keys<KS>(key, lane);
+  wave_lds_sync();
+#pragma unroll
+  for (int k = 0; k < KS; ++k) W[lane * KS + k] = key[k];
+}
+
+}  // namespace fs
