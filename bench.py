@@ -271,8 +271,19 @@ def time_decompose(torch, np, workload, fs, args) -> int:
         fs.cost_decompose(ta, tp, to, st, **kw)
     torch.cuda.synchronize()
     dt = (time.perf_counter() - t0) / args.steps
+    # algorithmic work: sorting the 2n start/end events (2 lane-ops per
+    # compare-exchange of a bitonic network) and O(1) per event for the state
+    # scans and span terms (4 lane-ops)
+    NP2 = 64
+    while NP2 < 2 * w.n_jobs:
+        NP2 *= 2
+    L = NP2.bit_length() - 1
+    ops = float(w.n_inst) * (2 * (NP2 // 2) * L * (L + 1) // 2 + 4 * 2 * w.n_jobs)
     print(json.dumps({"mode": "decompose", "workload": w.name, "ms_per_call": dt * 1e3,
-                      "instance_steps_per_s": steps_per_call / dt}))
+                      "instance_steps_per_s": steps_per_call / dt,
+                      "roofline": {"bound": "alu", "achieved": ops / dt / 1e12,
+                                   "peak": PEAK_ALU / 1e12, "frac": ops / dt / PEAK_ALU,
+                                   "ops_per_launch": ops}}))
     return 0
 
 
