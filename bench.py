@@ -81,11 +81,11 @@ def main() -> int:
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the per-alpha roofline lines of the fairness-budget sweep workload")
     ap.add_argument("--mode", default="simulate",
-                    choices=["simulate", "copy", "decompose", "opt", "host"],
+                    choices=["simulate", "copy", "decompose", "opt", "host", "profit"],
                     help="simulate: the benchmark line; copy: a plain device copy of known size "
                          "(calibrates the HBM byte counters); decompose / opt: time the other "
                          "two library calls (for profiles); host: host-buffer calls, "
-                         "PCIe copies included")
+                         "PCIe copies included; profit: the linear-pricing experiment")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the instances are "
@@ -106,6 +106,8 @@ def main() -> int:
         return time_opt(torch, np, workload, fs, args)
     if args.mode == "host":
         return time_host(torch, np, workload, fs, args)
+    if args.mode == "profit":
+        return time_profit(args)
     w = workload.WORKLOADS[args.workload]
     alpha = w.alphas[0]
     policy = "isjl"
@@ -236,6 +238,20 @@ def time_host(torch, np, workload, fs, args) -> int:
     print(json.dumps({"mode": "host", "workload": w.name, "ms_per_call": dt * 1e3,
                       "instance_steps_per_s": steps / dt,
                       "table_bytes": int(a.nbytes + p.nbytes + o.nbytes)}))
+    return 0
+
+
+def time_profit(args) -> int:
+    """The linear-pricing experiment (profit and cost decomposition, break-even
+    overhead): 5 replications x 9 policies through the library, timed."""
+    from paper_2608_02244_amd import profit
+    profit.run_table(profit.gpu_simulate, replications=1)  # warm-up
+    t0 = time.perf_counter()
+    res = profit.run_table(profit.gpu_simulate, replications=5)
+    dt = time.perf_counter() - t0
+    print(json.dumps({"mode": "profit", "seconds": dt, "calls": 45,
+                      "table": res["table"], "breakeven": {str(k): v for k, v in
+                                                           res["breakeven"].items()}}))
     return 0
 
 

@@ -189,3 +189,53 @@ def random_tables(rng: np.random.Generator, n_inst: int, n_jobs: int, max_prompt
     else:
         arr = np.zeros((n_inst, n_jobs), dtype=np.int32)
     return np.ascontiguousarray(arr), np.ascontiguousarray(pro), np.ascontiguousarray(out)
+
+
+# ---------------------------------------------------------------------------
+# The linear-pricing experiment of the paper's numerical section on profit and
+# cost alignment: n potential requests with lengths uniform on 1..o_max, each
+# quoted p0 * o (p0 = p / 500); a request in length bucket b (ten buckets of
+# width o_max / 10) accepts with probability max(0, 1 - k_b * price), where
+# k_b = 1 / (p0 (2b - 1) o_max / 10).  The accepted requests form one offline
+# instance (all released at step 0, no prompt part).  Draws come from
+# SplitMix64 keyed by (seed, replication): per request, the length, then the
+# acceptance uniform.
+
+_MASK64 = (1 << 64) - 1
+
+
+def _splitmix64(state: int):
+    while True:
+        state = (state + 0x9E3779B97F4A7C15) & _MASK64
+        z = state
+        z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & _MASK64
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & _MASK64
+        yield z ^ (z >> 31)
+
+
+def pricing_requests(replication: int, seed: int = 0, n: int = 400, o_max: int = 1000,
+                     p: float = 1.0):
+    """Return (lengths of the n potential requests, accepted mask, p0)."""
+    rnd = _splitmix64((seed * 0x100000001B3 + 7919 * replication + 0x5EED) & _MASK64)
+    p0 = p / 500.0
+    width = o_max // 10
+    lens = np.empty(n, dtype=np.int32)
+    acc = np.zeros(n, dtype=bool)
+    for i in range(n):
+        u = (next(rnd) >> 11) * (2.0 ** -53)
+        o = 1 + int(u * o_max)
+        b = (o + width - 1) // width
+        k_b = 1.0 / (p0 * (2 * b - 1) * width)
+        prob = max(0.0, 1.0 - k_b * p0 * o)
+        v = (next(rnd) >> 11) * (2.0 ** -53)
+        lens[i] = o
+        acc[i] = v < prob
+    return lens, acc, p0
+
+
+def pricing_instance(replication: int, seed: int = 0, n: int = 400):
+    """The accepted requests of one replication as a one-instance job table."""
+    lens, acc, _ = pricing_requests(replication, seed, n)
+    out = lens[acc].reshape(1, -1).astype(np.int32)
+    z = np.zeros_like(out)
+    return np.ascontiguousarray(z), np.ascontiguousarray(z), np.ascontiguousarray(out)
