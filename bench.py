@@ -249,9 +249,22 @@ def time_profit(args) -> int:
     t0 = time.perf_counter()
     res = profit.run_table(profit.gpu_simulate, replications=5)
     dt = time.perf_counter() - t0
+    # calibration replay of the fairness-budget sweep workload (4,096 x 2,000,
+    # B = 128, M_kv = 262,144) on a grid alpha = delta * Q / O
+    import workload
+    w = workload.WORKLOADS["bimodal_sweep_4096x2000"]
+    a, p, o = workload.generate(w)
+    deltas = (0.0, 0.01, 0.02, 0.05, 0.1, 0.2, 0.5, 1.0)
+    profit.calibrate_alpha(profit.gpu_simulate_batch, a[:64], p[:64], o[:64], deltas[:2],
+                           B=w.B, M_kv=w.M_kv)  # warm-up
+    t1 = time.perf_counter()
+    cal = profit.calibrate_alpha(profit.gpu_simulate_batch, a, p, o, deltas, B=w.B,
+                                 M_kv=w.M_kv, c=w.cost_c * 1e-6, tau=w.cost_tau * 1e-6)
+    dcal = time.perf_counter() - t1
     print(json.dumps({"mode": "profit", "seconds": dt, "calls": 45,
                       "table": res["table"], "breakeven": {str(k): v for k, v in
-                                                           res["breakeven"].items()}}))
+                                                           res["breakeven"].items()},
+                      "calibration": {"workload": w.name, "seconds": dcal, **cal}}))
     return 0
 
 

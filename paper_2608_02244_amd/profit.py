@@ -101,3 +101,61 @@ if __name__ == "__main__":
     import os
     sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
     print(format_table(run_table()))
+
+
+# ---------------------------------------------------------------------------
+# Calibration of the fairness budget by replay (the paper's practical
+# calibration procedure): every alpha-fair schedule has E <= alpha * O, so
+# alpha <= alpha_cost(delta) = delta * Q / O keeps the externality cost within
+# delta times the intrinsic cost; the operator replays a workload under ISJL on
+# a grid of alpha values scaled by Q / O and picks the alpha with the smallest
+# schedule-dependent cost c T + tau E, subject to service targets.
+
+
+def q_over_o(prompt, output) -> float:
+    """Q / O of a workload: sum len (len + 1) / 2 over sum len."""
+    ln = np.asarray(prompt, dtype=np.int64) + np.asarray(output, dtype=np.int64)
+    return float((ln * (ln + 1) // 2).sum()) / float(ln.sum())
+
+
+def alpha_cost(delta: float, prompt, output) -> float:
+    return delta * q_over_o(prompt, output)
+
+
+def gpu_simulate_batch(a, p, o, alpha: int, B: int, M_kv: int):
+    """All instances through the HIP library: (metrics, finish) on the host."""
+    from . import simulate
+    m, _, fi = simulate(a, p, o, policy="isjl", B=B, alpha=alpha, M_kv=M_kv, cost_c=0,
+                        cost_tau=0, schedule=True)
+    return m, fi
+
+
+def calibrate_alpha(simulate_batch: Callable, a, p, o, deltas: Sequence[float], B: int,
+                    M_kv: int = 0, c: float = 0.0005, tau: float = 1e-6,
+                    min_throughput: Optional[float] = None,
+                    latency_q: float = 0.95, max_latency_q: Optional[float] = None) -> Dict:
+    """Replay the workload (every instance) under ISJL for alpha = round(delta Q/O)
+    and return the grid with the chosen alpha.
+
+    Per alpha: schedule cost c * sum T + tau * sum E, throughput sum O / sum T,
+    the latency quantile over every job (finish - arrival), and whether
+    tau E <= delta tau Q holds (it must when alpha <= alpha_cost(delta))."""
+    qo = q_over_o(p, o)
+    arr = np.asarray(a, dtype=np.int64)
+    grid = []
+    for d in deltas:
+        al = int(d * qo)
+        m, fi = simulate_batch(a, p, o, al, B, M_kv)
+        T, O, Q, E = (float(m[f].astype(np.int64).sum()) for f in ("T", "O", "Q", "E"))
+        lat = np.asarray(fi, dtype=np.int64) - arr
+        grid.append({"delta": d, "alpha": al, "sched_cost": c * T + tau * E,
+                     "throughput": O / T, "latency_q": float(np.quantile(lat, latency_q)),
+                     "tauE": tau * E, "tauQ": tau * Q,
+                     "externality_within_delta": E <= d * Q,
+                     "E_within_alpha_O": bool((m["E"].astype(np.int64) <=
+                                               al * m["O"].astype(np.int64)).all())})
+    ok = [g for g in grid
+          if (min_throughput is None or g["throughput"] >= min_throughput)
+          and (max_latency_q is None or g["latency_q"] <= max_latency_q)]
+    best = min(ok, key=lambda g: (g["sched_cost"], g["alpha"])) if ok else None
+    return {"q_over_o": qo, "grid": grid, "alpha_star": None if best is None else best["alpha"]}

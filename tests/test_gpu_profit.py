@@ -23,3 +23,19 @@ def test_profit_table_matches_oracle():
                 assert int(g[f]) == int(r[f]), (k, f)
     assert got["table"] == ref["table"]
     assert got["breakeven"] == ref["breakeven"]
+
+
+def oracle_simulate_batch(a, p, o, alpha, B, M_kv):
+    m, _, fi = oracle.simulate(a, p, o, policy="isjl", B=B, alpha=alpha, M_kv=M_kv,
+                               cost_c=0, cost_tau=0, schedule=True)
+    return m, fi
+
+
+def test_alpha_calibration_matches_oracle():
+    import workload
+    a, p, o = workload.generate("bimodal_sweep_4096x2000", n_inst=8, n_jobs=400)
+    deltas = (0.0, 0.02, 0.05, 0.1, 0.3, 1.0)
+    got = profit.calibrate_alpha(profit.gpu_simulate_batch, a, p, o, deltas, B=128,
+                                 M_kv=262144)
+    ref = profit.calibrate_alpha(oracle_simulate_batch, a, p, o, deltas, B=128, M_kv=262144)
+    assert got == ref

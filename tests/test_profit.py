@@ -129,3 +129,35 @@ def test_pairwise_profit_difference_and_break_even():
                     d = profit.row_terms(r, c, 1e-6, 1 / 500)["profit"] - \
                         profit.row_terms(lj, c, 1e-6, 1 / 500)["profit"]
                     assert np.sign(d) == sgn * np.sign(dT)
+
+
+def oracle_simulate_batch(a, p, o, alpha, B, M_kv):
+    m, _, fi = oracle.simulate(a, p, o, policy="isjl", B=B, alpha=alpha, M_kv=M_kv,
+                               cost_c=0, cost_tau=0, schedule=True)
+    return m, fi
+
+
+def test_q_over_o_matches_the_token_sum():
+    """Q / O from the token-level sums (r = a + 1): sum_k k over each job."""
+    o = np.array([[1, 2, 3, 10]], np.int32)
+    p = np.zeros_like(o)
+    want = sum(sum(range(1, x + 1)) for x in (1, 2, 3, 10)) / 16
+    assert profit.q_over_o(p, o) == want
+    assert profit.alpha_cost(0.5, p, o) == 0.5 * want
+
+
+def test_alpha_calibration_replay_on_the_oracle():
+    """Every alpha-fair schedule has E <= alpha O, so at alpha = delta Q / O the
+    externality stays within delta Q; the chosen alpha minimises c T + tau E
+    among the grid points that meet the targets."""
+    a, p, o = workload.generate("lognormal_4096x1000", n_inst=6, n_jobs=120)
+    deltas = (0.0, 0.05, 0.1, 0.2, 0.5, 1.0)
+    res = profit.calibrate_alpha(oracle_simulate_batch, a, p, o, deltas, B=16, M_kv=20000)
+    for g in res["grid"]:
+        assert g["E_within_alpha_O"] and g["externality_within_delta"]
+    best = min(res["grid"], key=lambda g: (g["sched_cost"], g["alpha"]))
+    assert res["alpha_star"] == best["alpha"]
+    # a throughput target above every grid point leaves nothing to choose
+    top = max(g["throughput"] for g in res["grid"])
+    assert profit.calibrate_alpha(oracle_simulate_batch, a, p, o, deltas, B=16, M_kv=20000,
+                                  min_throughput=top * 1.01)["alpha_star"] is None
