@@ -81,11 +81,13 @@ def main() -> int:
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the per-alpha roofline lines of the fairness-budget sweep workload")
     ap.add_argument("--mode", default="simulate",
-                    choices=["simulate", "copy", "decompose", "opt", "host", "profit"],
+                    choices=["simulate", "copy", "decompose", "opt", "host", "profit",
+                             "gamma"],
                     help="simulate: the benchmark line; copy: a plain device copy of known size "
                          "(calibrates the HBM byte counters); decompose / opt: time the other "
                          "two library calls (for profiles); host: host-buffer calls, "
-                         "PCIe copies included; profit: the linear-pricing experiment")
+                         "PCIe copies included; profit: the linear-pricing experiment; "
+                         "gamma: the competitive-ratio experiment")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the instances are "
@@ -108,6 +110,8 @@ def main() -> int:
         return time_host(torch, np, workload, fs, args)
     if args.mode == "profit":
         return time_profit(args)
+    if args.mode == "gamma":
+        return time_gamma(args)
     w = workload.WORKLOADS[args.workload]
     alpha = w.alphas[0]
     policy = "isjl"
@@ -265,6 +269,24 @@ def time_profit(args) -> int:
                       "table": res["table"], "breakeven": {str(k): v for k, v in
                                                            res["breakeven"].items()},
                       "calibration": {"workload": w.name, "seconds": dcal, **cal}}))
+    return 0
+
+
+def time_gamma(args) -> int:
+    """Exact optimum against ISJL over the tiny workload, B = 2, alpha = 1..19,
+    binned by gamma = alpha / o_1, with beta = alpha and with beta*."""
+    import workload
+    from paper_2608_02244_amd import gamma_curve as gc
+    n = 262144
+    a, p, o = workload.generate("tiny_opt_1048576x8", n_inst=n)
+    alphas = list(range(1, 20))
+    out = {"mode": "gamma", "workload": "tiny_opt_1048576x8", "instances": n, "alphas": alphas}
+    for bs in (False, True):
+        t0 = time.perf_counter()
+        res = gc.run(gc.gpu_pair, a, p, o, alphas, B=2, beta_star=bs)
+        out["beta_star" if bs else "beta_alpha"] = {"seconds": time.perf_counter() - t0,
+                                                    **gc.to_json(res)}
+    print(json.dumps(out))
     return 0
 
 

@@ -428,7 +428,9 @@ def test_recorded_findings():
     - Theorem 3.3's curve CR(gamma) is not a lower bound at B = 2, beta = alpha;
     - with B = 3, where Algorithm 3's plan is fair only pairwise with o_1 and every
       plan start is guarded, T_OPT/T_ISJL falls to 1/2 < 3/4 (Theorem 3.3's and
-      Theorem 3.4's claims for B >= 2)."""
+      Theorem 3.4's claims for B >= 2);
+    - at B = 2 with beta = alpha the ratio falls to 26/35 < 3/4 (Theorem 3.1's
+      bound at beta = alpha)."""
     with open(os.path.join(GOLDEN, "cr_findings.json")) as fh:
         cases = json.load(fh)
     for c in cases:
