@@ -80,9 +80,14 @@ enum {
 enum {
   FSCHED_F_DEVICE_PTRS = 1u, /* array arguments are device pointers            */
   FSCHED_F_SYNC = 4u,        /* device mode: synchronize the stream before return */
-  FSCHED_F_BETA_SQRT17 = 8u  /* ISJL: beta = floor((sqrt(17)-1) alpha / 4), the
+  FSCHED_F_BETA_SQRT17 = 8u, /* ISJL: beta = floor((sqrt(17)-1) alpha / 4), the
                                 B = 2 choice of Section 3.2; default beta = alpha
                                 (Section 3.3)                                   */
+  FSCHED_F_RESUME_FILL = 16u /* ISJL, experiments only: after Phase TWO stops on
+                                A_max > alpha, it resumes as soon as A_max <= alpha
+                                again instead of waiting for the machine to empty
+                                (the other reading of "repeat from Phase ONE"
+                                with busy workers, Algorithms 2 and 3)          */
 };
 
 /* Scheduling and cost parameters (40 bytes, no padding). */

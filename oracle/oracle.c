@@ -47,6 +47,7 @@
 #define POL_SJF 3
 
 #define FLAG_BETA_SQRT17 8u
+#define FLAG_RESUME_FILL 16u
 
 #define ALPHA_INF_SENTINEL 2147483647
 
@@ -383,7 +384,11 @@ static void admit_isjl(or_sim* S, const int32_t* ord_long, int64_t t, int64_t am
   /* Phase TWO: an idle worker with nothing planned takes the longest released
    * unplanned job while A_max(t) <= alpha; otherwise stop admitting (DRAIN)
    * until the machine is empty and Phase ONE runs again. */
-  if (S->mode != 0) return;
+  if (S->mode != 0) {
+    /* Reading flag (experiments only): resume as soon as A_max(t) <= alpha. */
+    if ((flags & FLAG_RESUME_FILL) && amax <= I->alpha) S->mode = 0;
+    else return;
+  }
   for (int64_t w = 0; w < I->B; ++w) {
     if (S->cur[w] >= 0 || S->qhead[w] >= 0) continue;
     int32_t j = longest_pool_job(S, ord_long, t);

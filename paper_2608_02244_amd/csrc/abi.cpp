@@ -39,7 +39,8 @@ int check_params(const fsched_params* p, bool need_policy) {
   if (p->B < 0 || p->alpha < 0 || p->M_kv < 0 || p->cost_c < 0 || p->cost_tau < 0)
     return FSCHED_EINVAL;
   if (need_policy && (p->policy < FSCHED_FCFS || p->policy > FSCHED_SJF)) return FSCHED_EINVAL;
-  const uint32_t known = FSCHED_F_DEVICE_PTRS | FSCHED_F_SYNC | FSCHED_F_BETA_SQRT17;
+  const uint32_t known =
+      FSCHED_F_DEVICE_PTRS | FSCHED_F_SYNC | FSCHED_F_BETA_SQRT17 | FSCHED_F_RESUME_FILL;
   if (p->flags & ~known) return FSCHED_EINVAL;
   return FSCHED_OK;
 }
@@ -110,6 +111,7 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
   a.Beff = Beff;
   a.alpha = p->alpha;
   a.beta = (p->flags & FSCHED_F_BETA_SQRT17) ? beta_sqrt17(p->alpha) : p->alpha;
+  a.resume = (p->flags & FSCHED_F_RESUME_FILL) ? 1 : 0;
   a.M = p->M_kv;
   a.c = p->cost_c;
   a.tau = p->cost_tau;

@@ -30,7 +30,8 @@ struct SimArgs {
   int32_t off_arr;    // word offset of arrival-by-rank (general kernel)
   int32_t off_q;      // word offset of the plan-queue links (ISJL)
   int32_t off_stage;  // word offset of the gather / release buffer (not FCFS)
-  int32_t pad;
+  int32_t resume;     // ISJL: Phase TWO resumes once A_max <= alpha (1) or waits
+                      // for an empty machine (0)
   const int32_t* arrival;
   const int32_t* prompt;
   const int32_t* output;

@@ -852,7 +852,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
         }
       }
       // Phase TWO (FILL): idle workers with nothing planned take the longest
-      // queued unplanned job while A_max(t) <= alpha; otherwise DRAIN.
+      // queued unplanned job while A_max(t) <= alpha; otherwise DRAIN (until
+      // the machine is empty, or with the resume reading until A_max <= alpha).
+      if (mode == 1 && a.resume && amax <= alpha) mode = 0;
       if (mode == 0) {
         // idle workers with an empty plan queue (all idle ones when nothing is planned)
         int nie = Beff - S.nact;
@@ -1013,7 +1015,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
         // the machine is empty or A_max <= alpha (A_max right after the
         // completions at e is e - t + the largest progress still active).
         stop = quiet >= 3 ? quiet - 1 : N - 1;
-        if (POL == POL_ISJL && planned > 0) {
+        if (POL == POL_ISJL && (planned > 0 || (a.resume && mode == 1))) {
           int cg_max = xs_max, lfound = IDLE;
 #pragma unroll
           for (int k = KS - 1; k >= 0; --k) {

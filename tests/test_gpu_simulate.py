@@ -278,3 +278,34 @@ def test_long_jobs(dev, policy):
         log(f"long jobs {policy} B={B} alpha={alpha}")
         check(dev, f"long {policy} B={B} alpha={alpha}", a, p, o, policy=policy, B=B,
               alpha=alpha, M_kv=0, cost_c=3, cost_tau=1)
+
+
+def test_resume_fill_reading(dev):
+    """The experiment flag (Phase TWO resumes once A_max <= alpha) against the
+    oracle with the same flag: small random instances and a full-size sample."""
+    rng = np.random.default_rng(zlib.crc32(b"resume"))
+    for trial in range(18):
+        n = int(rng.choice([7, 64, 130, 300]))
+        B = int(rng.choice([3, 5, 8, 0]))
+        alpha = int(rng.choice([1, 4, 15, 60]))
+        mode = trial % 3
+        a, p, o = workload.random_tables(rng, 16, n, int(rng.choice([0, 8])), 40,
+                                         max_arrival=0 if mode == 0 else 300,
+                                         sorted_arrivals=(mode == 1))
+        M_kv = int(rng.choice([0, 0, 400]))
+        ctx = f"resume n={n} B={B} alpha={alpha} M={M_kv} mode={mode}"
+        log(ctx)
+        got, gs, gf = gpu_sim(dev, a, p, o, policy="isjl", B=B, alpha=alpha, M_kv=M_kv,
+                              cost_c=3, cost_tau=1, resume_fill=True)
+        ref, rs, rf = oracle.simulate(a, p, o, policy="isjl", B=B, alpha=alpha, M_kv=M_kv,
+                                      cost_c=3, cost_tau=1, schedule=True,
+                                      flags=oracle.FLAG_RESUME_FILL)
+        assert_same(ctx, got, ref, gs, rs, gf, rf)
+    w = workload.WORKLOADS["lognormal_4096x1000"]
+    a, p, o = workload.generate(w, n_inst=48)
+    log("resume lognormal_4096x1000 sample")
+    kw = dict(policy="isjl", B=w.B, alpha=w.alphas[0], M_kv=w.M_kv, cost_c=w.cost_c,
+              cost_tau=w.cost_tau)
+    got, gs, gf = gpu_sim(dev, a, p, o, resume_fill=True, **kw)
+    ref, rs, rf = oracle.simulate(a, p, o, schedule=True, flags=oracle.FLAG_RESUME_FILL, **kw)
+    assert_same("resume lognormal sample", got, ref, gs, rs, gf, rf)

@@ -486,3 +486,29 @@ def test_invalid_inputs_rejected():
         oracle.simulate(z(2), z(2), arr([1, 0]), policy="fcfs", B=1, alpha=0)
     with pytest.raises(oracle.OracleError):
         oracle.opt(z(9), z(9), np.ones(9, np.int32), B=2, alpha=1)
+
+
+def test_resume_fill_reading():
+    """The experiment flag that resumes Phase TWO once A_max <= alpha: with B = 2
+    it changes nothing (the job left running keeps A_max > alpha until it ends),
+    every step stays within alpha, and for B > 2 it can only admit more."""
+    rng = np.random.default_rng(16)
+    changed = 0
+    for trial in range(40):
+        n = int(rng.integers(2, 40))
+        a, p, o = random_tables(rng, 8, n, 3, 30,
+                                         max_arrival=int(rng.choice([0, 40])),
+                                         sorted_arrivals=bool(trial % 2))
+        for B in (1, 2, 3, 6):
+            alpha = int(rng.integers(0, 25))
+            kw = dict(policy="isjl", B=B, alpha=alpha, M_kv=int(rng.choice([0, 60])),
+                      cost_c=1, cost_tau=1)
+            m0 = oracle.simulate(a, p, o, **kw)
+            m1 = oracle.simulate(a, p, o, flags=oracle.FLAG_RESUME_FILL, **kw)
+            assert (m1["unfair_steps"] == 0).all() and (m1["max_extent"] <= alpha).all()
+            if B <= 2:
+                for f in m0.dtype.names:
+                    assert np.array_equal(m0[f], m1[f]), (B, f)
+            else:
+                changed += int((m0["T"] != m1["T"]).sum())
+    assert changed > 0
