@@ -63,9 +63,12 @@ def _load():
         P, I32, I64, U32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32
         lib.oracle_simulate_batch.argtypes = [I64, I32, P, P, P, I32, I32, I64, I32, U32, I64,
                                               I64, P, P, P]
+        lib.oracle_simulate_robust_batch.argtypes = [I64, I32, P, P, P, P, I32, I32, I64, I32,
+                                                     U32, I64, I64, P, P, P]
         lib.oracle_decompose.argtypes = [I32, P, P, P, I32, I32, I64, I64, I64, P, P, P]
         lib.oracle_opt_batch.argtypes = [I64, I32, P, P, P, I32, I32, I64, P, P]
-        for f in (lib.oracle_simulate_batch, lib.oracle_decompose, lib.oracle_opt_batch):
+        for f in (lib.oracle_simulate_batch, lib.oracle_simulate_robust_batch,
+                  lib.oracle_decompose, lib.oracle_opt_batch):
             f.restype = ctypes.c_int
         assert lib.oracle_metrics_size() == 104
         _lib = lib
@@ -98,6 +101,26 @@ def simulate(arrival, prompt, output, *, policy: str, B: int, alpha: int, M_kv: 
     rc = _load().oracle_simulate_batch(n_inst, n, a.ctypes.data, p.ctypes.data, o.ctypes.data,
                                        B, alpha, M_kv, POLICIES[policy], flags, cost_c,
                                        cost_tau, out.ctypes.data, _ptr(st), _ptr(fi))
+    if rc:
+        raise OracleError(rc)
+    return (out, st, fi) if schedule else out
+
+
+def simulate_robust(arrival, prompt, output, upper, *, policy: str = "isjl", B: int,
+                    alpha: int, M_kv: int = 0, cost_c: int = 0, cost_tau: int = 1,
+                    flags: int = 0, schedule: bool = False):
+    """Simulate with planning sizes prompt + upper (Section 3.5; upper >= output):
+    ISJL gives Robust-ISJL.  Returns as ``simulate``."""
+    a, p, o = _tables(arrival, prompt, output)
+    u = np.ascontiguousarray(upper, dtype=np.int32).reshape(a.shape)
+    n_inst, n = a.shape
+    out = np.zeros(n_inst, dtype=METRICS_DTYPE)
+    st = np.empty((n_inst, n), np.int32) if schedule else None
+    fi = np.empty((n_inst, n), np.int32) if schedule else None
+    rc = _load().oracle_simulate_robust_batch(n_inst, n, a.ctypes.data, p.ctypes.data,
+                                              o.ctypes.data, u.ctypes.data, B, alpha, M_kv,
+                                              POLICIES[policy], flags, cost_c, cost_tau,
+                                              out.ctypes.data, _ptr(st), _ptr(fi))
     if rc:
         raise OracleError(rc)
     return (out, st, fi) if schedule else out

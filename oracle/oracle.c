@@ -68,6 +68,8 @@ typedef struct {
   int64_t c, tau;
   const int32_t* arrival;
   int64_t* len;       /* service length = prompt + output         */
+  int64_t* plan;      /* planning size: len, or prompt + the predicted upper
+                         bound of the output (Robust-ISJL, Section 3.5) */
 } or_inst;
 
 /* ------------------------------------------------------------------ */
@@ -158,7 +160,7 @@ static int cmp_order(const void* pa, const void* pb) {
 
 static void make_order(int32_t* ord, const or_inst* I, int mode) {
   for (int32_t i = 0; i < I->n; ++i) ord[i] = i;
-  g_key1 = I->len;
+  g_key1 = I->plan;
   g_key1i = I->arrival;
   g_key_mode = mode;
   qsort(ord, (size_t)I->n, sizeof(int32_t), cmp_order);
@@ -193,14 +195,14 @@ typedef struct {
  * a job that would run alone is always admissible). */
 static int kv_ok(const or_sim* S, int32_t j) {
   if (S->I->M == 0 || S->nact == 0) return 1;
-  return S->res + S->I->len[j] <= S->I->M;
+  return S->res + S->I->plan[j] <= S->I->M;
 }
 
 static void admit(or_sim* S, int32_t j, int64_t t) {
   S->st[j] = ST_ACTIVE;
   S->start[j] = t;
   S->act[S->nact++] = j;
-  S->res += S->I->len[j];
+  S->res += S->I->plan[j];
 }
 
 static int released(const or_inst* I, int32_t j, int64_t t) { return I->arrival[j] <= t; }
@@ -289,26 +291,26 @@ static void phase_one(or_sim* S, const int32_t* ord_long, int64_t t, uint32_t fl
    * ISJL identical to LJF. */
   int64_t Bp = 0, resv = 0;
   for (int32_t q = 0; q < k && Bp < I->B; ++q) {
-    int64_t L = I->len[S->pool[q]];
+    int64_t L = I->plan[S->pool[q]];
     if (I->M != 0 && q > 0 && resv + L > I->M) break;
     resv += L;
     Bp++;
   }
   /* "if o_2 <= alpha, go to Phase TWO" (also: a single job, or one worker) */
-  if (k == 1 || Bp == 1 || I->len[S->pool[1]] <= a) return;
+  if (k == 1 || Bp == 1 || I->plan[S->pool[1]] <= a) return;
   /* M = min{B, #{o_i > alpha}}; o_1 > o_2 > alpha so M >= 2 */
   int64_t m = 0;
   for (int32_t q = 0; q < k; ++q)
-    if (I->len[S->pool[q]] > a) m++;
+    if (I->plan[S->pool[q]] > a) m++;
   if (m > Bp) m = Bp;
   const int64_t beta = (flags & FLAG_BETA_SQRT17) ? beta_sqrt17(a) : a;
-  const int64_t o1 = I->len[S->pool[0]];
+  const int64_t o1 = I->plan[S->pool[0]];
   /* cap_j = min{2 alpha, o_1 - o_j + beta} for the long workers j = 2..M;
    * the spare workers j = M+1..Bp take packs of total at most alpha. */
   for (int64_t w = 0; w < Bp; ++w) {
     S->load[w] = 0;
     if (w >= 1 && w < m) {
-      int64_t c1 = 2 * a, c2 = o1 - I->len[S->pool[w]] + beta;
+      int64_t c1 = 2 * a, c2 = o1 - I->plan[S->pool[w]] + beta;
       S->cap[w] = c1 < c2 ? c1 : c2;
     } else {
       S->cap[w] = a;
@@ -320,7 +322,7 @@ static void phase_one(or_sim* S, const int32_t* ord_long, int64_t t, uint32_t fl
    * largest index with room. */
   for (int32_t q = (int32_t)m; q < k; ++q) {
     int32_t j = S->pool[q];
-    int64_t L = I->len[j];
+    int64_t L = I->plan[j];
     int64_t placed = -1;
     for (int64_t w = m; w < Bp; ++w)
       if (S->load[w] + L <= a) {
@@ -431,6 +433,7 @@ static int make_inst(or_inst* I, int32_t n, const int32_t* arrival, const int32_
   I->len = (int64_t*)malloc(sizeof(int64_t) * (size_t)n);
   if (!I->len) return OR_ENOMEM;
   for (int32_t i = 0; i < n; ++i) I->len[i] = (int64_t)prompt[i] + output[i];
+  I->plan = I->len;
   return OR_OK;
 }
 
@@ -439,15 +442,35 @@ static int make_inst(or_inst* I, int32_t n, const int32_t* arrival, const int32_
  * A_max(t) = max progress of the still-active jobs; let the policy admit jobs
  * released by t (they start with progress 0); account the step.  The run ends
  * when every job has finished; T is the makespan (idle steps included). */
-int oracle_simulate(int32_t n, const int32_t* arrival, const int32_t* prompt,
-                    const int32_t* output, int32_t B, int32_t alpha, int64_t M_kv,
-                    int32_t policy, uint32_t flags, int64_t cost_c, int64_t cost_tau,
-                    or_metrics* out, int32_t* start_out, int32_t* finish_out) {
+static int simulate_impl(int32_t n, const int32_t* arrival, const int32_t* prompt,
+                         const int32_t* output, const int32_t* upper, int32_t B, int32_t alpha,
+                         int64_t M_kv, int32_t policy, uint32_t flags, int64_t cost_c,
+                         int64_t cost_tau, or_metrics* out, int32_t* start_out,
+                         int32_t* finish_out) {
   if (!out) return OR_EINVAL;
   if (policy < 0 || policy > 3) return OR_EINVAL;
   or_inst I;
   int rc = make_inst(&I, n, arrival, prompt, output, B, alpha, M_kv, cost_c, cost_tau);
   if (rc) return rc;
+  if (upper) {
+    /* Robust-ISJL (Section 3.5): sizes used for ordering, packing, M, the caps
+     * and (reading) the KV reservation are prompt + the predicted upper bound
+     * of the output; jobs still run their true length. */
+    I.plan = (int64_t*)malloc(sizeof(int64_t) * (size_t)n);
+    if (!I.plan) {
+      free(I.len);
+      return OR_ENOMEM;
+    }
+    for (int32_t i = 0; i < n; ++i) {
+      if (upper[i] < output[i] || (int64_t)prompt[i] + upper[i] > (1 << 30)) {
+        const int code = upper[i] < output[i] ? OR_EINVAL : OR_ERANGE;
+        free(I.plan);
+        free(I.len);
+        return code;
+      }
+      I.plan[i] = (int64_t)prompt[i] + upper[i];
+    }
+  }
   size_t nn = (size_t)n, nb = (size_t)I.B;
   or_sim S;
   memset(&S, 0, sizeof(S));
@@ -487,8 +510,8 @@ int oracle_simulate(int32_t n, const int32_t* arrival, const int32_t* prompt,
   int64_t max_r = 0, sum_len = 0, max_len = 0;
   for (int32_t i = 0; i < n; ++i) {
     if (arrival[i] > max_r) max_r = arrival[i];
-    sum_len += I.len[i];
-    if (I.len[i] > max_len) max_len = I.len[i];
+    sum_len += I.plan[i];
+    if (I.plan[i] > max_len) max_len = I.plan[i];
   }
   int64_t a_cap = I.alpha < max_len ? I.alpha : max_len;
   const int64_t bound = max_r + 2 * sum_len + (int64_t)n * a_cap + 2;
@@ -504,7 +527,7 @@ int oracle_simulate(int32_t n, const int32_t* arrival, const int32_t* prompt,
       int32_t j = S.act[k];
       if (S.start[j] + I.len[j] == t) {
         S.st[j] = ST_DONE;
-        S.res -= I.len[j];
+        S.res -= I.plan[j];
         ndone++;
         if (policy == POL_ISJL) S.cur[S.wk[j]] = -1;
       } else {
@@ -557,6 +580,7 @@ done:
   free(S.qnext);
   free(S.planned);
   free(S.pool);
+  if (I.plan != I.len) free(I.plan);
   free(I.len);
   return rc;
 }
@@ -879,6 +903,26 @@ int oracle_opt(int32_t n, const int32_t* arrival, const int32_t* prompt, const i
   return OR_OK;
 }
 
+int oracle_simulate(int32_t n, const int32_t* arrival, const int32_t* prompt,
+                    const int32_t* output, int32_t B, int32_t alpha, int64_t M_kv,
+                    int32_t policy, uint32_t flags, int64_t cost_c, int64_t cost_tau,
+                    or_metrics* out, int32_t* start_out, int32_t* finish_out) {
+  return simulate_impl(n, arrival, prompt, output, NULL, B, alpha, M_kv, policy, flags, cost_c,
+                       cost_tau, out, start_out, finish_out);
+}
+
+/* Robust-ISJL and the other policies on predicted sizes: upper[i] >= output[i]
+ * is the upper end of output i's prediction interval. */
+int oracle_simulate_robust(int32_t n, const int32_t* arrival, const int32_t* prompt,
+                           const int32_t* output, const int32_t* upper, int32_t B,
+                           int32_t alpha, int64_t M_kv, int32_t policy, uint32_t flags,
+                           int64_t cost_c, int64_t cost_tau, or_metrics* out,
+                           int32_t* start_out, int32_t* finish_out) {
+  if (!upper) return OR_EINVAL;
+  return simulate_impl(n, arrival, prompt, output, upper, B, alpha, M_kv, policy, flags, cost_c,
+                       cost_tau, out, start_out, finish_out);
+}
+
 /* Convenience loops over instances (still single-threaded). */
 int oracle_simulate_batch(int64_t n_inst, int32_t n, const int32_t* arrival,
                           const int32_t* prompt, const int32_t* output, int32_t B,
@@ -891,6 +935,23 @@ int oracle_simulate_batch(int64_t n_inst, int32_t n, const int32_t* arrival,
                              policy, flags, cost_c, cost_tau, out + k,
                              start_out ? start_out + off : NULL,
                              finish_out ? finish_out + off : NULL);
+    if (rc) return rc;
+  }
+  return OR_OK;
+}
+
+int oracle_simulate_robust_batch(int64_t n_inst, int32_t n, const int32_t* arrival,
+                                 const int32_t* prompt, const int32_t* output,
+                                 const int32_t* upper, int32_t B, int32_t alpha, int64_t M_kv,
+                                 int32_t policy, uint32_t flags, int64_t cost_c,
+                                 int64_t cost_tau, or_metrics* out, int32_t* start_out,
+                                 int32_t* finish_out) {
+  for (int64_t k = 0; k < n_inst; ++k) {
+    size_t off = (size_t)k * (size_t)n;
+    int rc = oracle_simulate_robust(n, arrival + off, prompt + off, output + off, upper + off,
+                                    B, alpha, M_kv, policy, flags, cost_c, cost_tau, out + k,
+                                    start_out ? start_out + off : NULL,
+                                    finish_out ? finish_out + off : NULL);
     if (rc) return rc;
   }
   return OR_OK;

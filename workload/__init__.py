@@ -239,3 +239,18 @@ def pricing_instance(replication: int, seed: int = 0, n: int = 400):
     out = lens[acc].reshape(1, -1).astype(np.int32)
     z = np.zeros_like(out)
     return np.ascontiguousarray(z), np.ascontiguousarray(z), np.ascontiguousarray(out)
+
+
+def prediction_upper(output, slack: float, seed: int = 0, tight: bool = False) -> np.ndarray:
+    """Upper ends u_i >= o_i of output-length prediction intervals (inputs of
+    Robust-ISJL): u_i = o_i + floor(U_i * slack * o_i) with U_i uniform on [0, 1)
+    from a seeded PCG64 stream, or U_i = 1 with ``tight`` (u_i = floor((1 +
+    slack) o_i), the interval of the scale-normalised corollary).  Same shape as
+    ``output``, int32."""
+    o = np.asarray(output, dtype=np.int64)
+    if tight:
+        u = np.ones(o.shape)
+    else:
+        u = np.random.Generator(np.random.PCG64(seed)).random(o.shape)
+    e = np.floor(u * float(slack) * o).astype(np.int64)
+    return (o + e).astype(np.int32)
