@@ -7,7 +7,9 @@ ordering, event loop, admissions, Section 5 accounting and the per-instance
 metrics, with the job tables already resident in HBM.  An instance-step is one
 logical step of one instance, so a step contributes sum_i T_i instance-steps.
 
-Prints one JSON line (see the design doc for the roofline definition).
+Prints one JSON line: the metric, the simulate kernel's position against the
+int32 VALU peak (algorithmic lane operations per launch over the measured launch
+time) and the single-core oracle's rate on a sample of the same workload.
 """
 from __future__ import annotations
 
@@ -54,7 +56,7 @@ def measured_traffic():
 
 
 def algorithmic_ops(n_inst: int, n: int, B: int, policy: str, sorted_arrivals: bool) -> float:
-    """Lane operations the event-driven method needs per launch (roofline):
+    """Lane operations the event-driven method needs per launch:
     ordering by a bitonic network (2 per compare-exchange), and per job one
     admission and one completion, each scanning the B-slot active table once
     (B compares) plus the table reductions after the completion (B), and one rank
@@ -82,17 +84,19 @@ def main() -> int:
                     help="skip the per-alpha roofline lines of the fairness-budget sweep workload")
     ap.add_argument("--mode", default="simulate",
                     choices=["simulate", "copy", "decompose", "opt", "host", "profit",
-                             "gamma"],
+                             "gamma", "robust"],
                     help="simulate: the benchmark line; copy: a plain device copy of known size "
                          "(calibrates the HBM byte counters); decompose / opt: time the other "
                          "two library calls (for profiles); host: host-buffer calls, "
                          "PCIe copies included; profit: the linear-pricing experiment; "
-                         "gamma: the competitive-ratio experiment")
+                         "gamma: the competitive-ratio experiment; robust: Robust-ISJL on "
+                         "predicted sizes (headline workload and the guarantee on tiny "
+                         "instances)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the instances are "
-              "independent, so more GPUs would each take a contiguous share of them "
-              "(see DESIGN.md), but this build measures one GPU.", file=sys.stderr)
+              "independent, so more GPUs would each take a contiguous share of them, but "
+              "only the one-GPU case is implemented and measured.", file=sys.stderr)
         return 2
 
     import numpy as np
@@ -112,6 +116,8 @@ def main() -> int:
         return time_profit(args)
     if args.mode == "gamma":
         return time_gamma(args)
+    if args.mode == "robust":
+        return time_robust(torch, np, workload, fs, args)
     w = workload.WORKLOADS[args.workload]
     alpha = w.alphas[0]
     policy = "isjl"
@@ -286,6 +292,67 @@ def time_gamma(args) -> int:
         res = gc.run(gc.gpu_pair, a, p, o, alphas, B=2, beta_star=bs)
         out["beta_star" if bs else "beta_alpha"] = {"seconds": time.perf_counter() - t0,
                                                     **gc.to_json(res)}
+    print(json.dumps(out))
+    return 0
+
+
+def time_robust(torch, np, workload, fs, args) -> int:
+    """Robust-ISJL: (1) the headline workload with upper bounds u = o + U * slack * o
+    at several slacks, timed like the benchmark line, against ISJL on the true
+    sizes (makespan and cost ratios, fairness); (2) the guarantee
+    T_R <= 4/3 (T_OPT + Delta_pack), its corollary and the proof's first step on
+    tiny offline instances."""
+    from paper_2608_02244_amd import robust as rb
+    w = workload.WORKLOADS[args.workload]
+    alpha = w.alphas[0]
+    dev = torch.device("cuda:0")
+    a, p, o = workload.generate(w)
+    ta, tp, to = (torch.from_numpy(x).to(dev) for x in (a, p, o))
+    kw = dict(B=w.B, alpha=alpha, M_kv=w.M_kv, cost_c=w.cost_c, cost_tau=w.cost_tau)
+    stream = torch.cuda.current_stream()
+    base = fs.metrics_view(fs.simulate(ta, tp, to, policy="isjl", **kw)[0])
+    rows = []
+    for slack in (0.0, 0.25, 1.0, 3.0):
+        tu = torch.from_numpy(workload.prediction_upper(o, slack, seed=1)).to(dev)
+        m = fs.metrics_view(fs.simulate_robust(ta, tp, to, tu, **kw)[0])
+        if (m["T"] < 0).any():
+            raise RuntimeError("some instance reported an error marker")
+        for _ in range(args.warmup):
+            fs.simulate_robust(ta, tp, to, tu, **kw)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            fs.simulate_robust(ta, tp, to, tu, **kw)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        print(f"robust headline slack={slack}: {ms:.2f} ms", file=sys.stderr, flush=True)
+        rows.append({"slack": slack, "ms_per_launch": ms,
+                     "instance_steps_per_s": float(m["T"].sum()) / (ms / 1e3),
+                     "T_over_isjl": float(m["T"].sum() / base["T"].sum()),
+                     "C_over_isjl": float(m["C"].sum() / base["C"].sum()),
+                     "latency_over_isjl": float(m["sum_latency"].sum() /
+                                                base["sum_latency"].sum()),
+                     "unfair_steps": int(m["unfair_steps"].sum()),
+                     "max_extent": int(m["max_extent"].max())})
+        del tu
+    out = {"mode": "robust", "workload": w.name, "alpha": alpha, "headline": rows}
+    # the exhaustive optimum gets much slower with B, so fewer instances there
+    tiny = []
+    for B, n in ((2, 32768), (3, 4096), (4, 1024)):
+        a, p, o = workload.generate("tiny_opt_1048576x8", n_inst=n)
+        for slack in (0.25, 1.0, 3.0):
+            u = workload.prediction_upper(o, slack, seed=5)
+            rows = []
+            for al in (1, 2, 4, 7, 11):
+                t0 = time.perf_counter()
+                rows += rb.run(rb.gpu_quad, a, p, o, u, [al], B=B)["rows"]
+                rows[-1]["seconds"] = time.perf_counter() - t0
+                print(f"robust tiny B={B} n={n} slack={slack} alpha={al}: "
+                      f"{rows[-1]['seconds']:.1f} s", file=sys.stderr, flush=True)
+            tiny.append({"B": B, "instances": n, "slack": slack, "rows": rows})
+    out["tiny"] = {"workload": "tiny_opt_1048576x8", "runs": tiny}
     print(json.dumps(out))
     return 0
 

@@ -159,6 +159,27 @@ int fsched_simulate(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
                     const int32_t* arrival, const int32_t* prompt, const int32_t* output,
                     fsched_metrics* out, int32_t* start, int32_t* finish, void* stream);
 
+/* fsched_simulate_robust — Robust-ISJL (Section 3.4): ISJL run with the proxy
+ * size prompt_i + upper_i wherever a job size is used to plan — the priority
+ * order, Phase ONE's M, caps and packs, worker 1's delay — and (reading: the
+ * size known at admission) for the KV reservation against M_kv.  Each job
+ * still runs prompt_i + output_i steps, and the fairness guard A_max(t) <=
+ * alpha uses the true progress, so the schedule is alpha-fair for any upper
+ * (the fairness theorem of Section 3.4).
+ * With upper == output the result equals fsched_simulate under ISJL.
+ *   upper    [n_inst][n_jobs] int32, upper_i >= output_i (upper end of the
+ *            prediction interval of output i; a smaller one is an invalid
+ *            table: EINVAL in host mode, T = FSCHED_T_INVALID in device mode).
+ *            prompt_i + upper_i is subject to the same length limit as the
+ *            true length (ETOOLARGE / FSCHED_T_TOOLARGE beyond it).
+ * p->policy must be FSCHED_ISJL (ENOTIMPL otherwise).  All other arguments,
+ * outputs and errors as fsched_simulate; metrics describe the true run. */
+int fsched_simulate_robust(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
+                           const int32_t* arrival, const int32_t* prompt,
+                           const int32_t* output, const int32_t* upper,
+                           fsched_metrics* out, int32_t* start, int32_t* finish,
+                           void* stream);
+
 /* fsched_cost_decompose — re-score given schedules (start steps) from the
  * schedule alone (Section 5 terms as in fsched_metrics) and check them.
  *   start      [n_inst][n_jobs] int32 start steps.

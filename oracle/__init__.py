@@ -109,7 +109,7 @@ def simulate(arrival, prompt, output, *, policy: str, B: int, alpha: int, M_kv: 
 def simulate_robust(arrival, prompt, output, upper, *, policy: str = "isjl", B: int,
                     alpha: int, M_kv: int = 0, cost_c: int = 0, cost_tau: int = 1,
                     flags: int = 0, schedule: bool = False):
-    """Simulate with planning sizes prompt + upper (Section 3.5; upper >= output):
+    """Simulate with planning sizes prompt + upper (Section 3.4; upper >= output):
     ISJL gives Robust-ISJL.  Returns as ``simulate``."""
     a, p, o = _tables(arrival, prompt, output)
     u = np.ascontiguousarray(upper, dtype=np.int32).reshape(a.shape)

@@ -69,7 +69,7 @@ typedef struct {
   const int32_t* arrival;
   int64_t* len;       /* service length = prompt + output         */
   int64_t* plan;      /* planning size: len, or prompt + the predicted upper
-                         bound of the output (Robust-ISJL, Section 3.5) */
+                         bound of the output (Robust-ISJL, Section 3.4) */
 } or_inst;
 
 /* ------------------------------------------------------------------ */
@@ -453,7 +453,7 @@ static int simulate_impl(int32_t n, const int32_t* arrival, const int32_t* promp
   int rc = make_inst(&I, n, arrival, prompt, output, B, alpha, M_kv, cost_c, cost_tau);
   if (rc) return rc;
   if (upper) {
-    /* Robust-ISJL (Section 3.5): sizes used for ordering, packing, M, the caps
+    /* Robust-ISJL (Section 3.4): sizes used for ordering, packing, M, the caps
      * and (reading) the KV reservation are prompt + the predicted upper bound
      * of the output; jobs still run their true length. */
     I.plan = (int64_t*)malloc(sizeof(int64_t) * (size_t)n);

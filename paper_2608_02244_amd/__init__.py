@@ -33,7 +33,7 @@ METRIC_FIELDS = ("T", "O", "Q", "E", "C", "W", "sum_completion", "sum_latency", 
 METRICS_DTYPE = np.dtype([(f, np.int64) for f in METRIC_FIELDS[:12]] +
                          [("max_extent", np.int32), ("max_active", np.int32)])
 METRICS_BYTES = 104
-EXPORTS = ("fsched_simulate", "fsched_cost_decompose", "fsched_bruteforce_opt",
+EXPORTS = ("fsched_simulate", "fsched_simulate_robust", "fsched_cost_decompose", "fsched_bruteforce_opt",
            "fsched_strerror", "fsched_abi_version", "fsched_last_hip_error")
 
 
@@ -66,9 +66,10 @@ def lib():
         L = ctypes.CDLL(LIB_PATH)
         P, I64, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
         L.fsched_simulate.argtypes = [P, I64, I32, P, P, P, P, P, P, P]
+        L.fsched_simulate_robust.argtypes = [P, I64, I32, P, P, P, P, P, P, P, P]
         L.fsched_cost_decompose.argtypes = [P, I64, I32, P, P, P, P, P, P, P]
         L.fsched_bruteforce_opt.argtypes = [P, I64, I32, P, P, P, P, P, P]
-        for f in (L.fsched_simulate, L.fsched_cost_decompose, L.fsched_bruteforce_opt,
+        for f in (L.fsched_simulate, L.fsched_simulate_robust, L.fsched_cost_decompose, L.fsched_bruteforce_opt,
                   L.fsched_abi_version, L.fsched_last_hip_error):
             f.restype = ctypes.c_int
         L.fsched_strerror.restype = ctypes.c_char_p
@@ -98,24 +99,24 @@ def _is_torch(x) -> bool:
     return hasattr(x, "data_ptr") and hasattr(x, "is_cuda")
 
 
-def _torch_tables(arrival, prompt, output):
+def _torch_tables(*tables):
     import torch
     ts = []
-    for x in (arrival, prompt, output):
+    for x in tables:
         if x.dtype != torch.int32 or not x.is_contiguous() or not x.is_cuda:
             raise ValueError("job tables must be contiguous int32 tensors on the GPU")
         ts.append(x if x.dim() == 2 else x.reshape(1, -1))
-    if not (ts[0].shape == ts[1].shape == ts[2].shape):
+    if any(x.shape != ts[0].shape for x in ts):
         raise ValueError("job tables differ in shape")
     return ts
 
 
-def _np_tables(arrival, prompt, output):
+def _np_tables(*tables):
     out = []
-    for x in (arrival, prompt, output):
+    for x in tables:
         a = np.ascontiguousarray(x, dtype=np.int32)
         out.append(a if a.ndim == 2 else a.reshape(1, -1))
-    if not (out[0].shape == out[1].shape == out[2].shape):
+    if any(x.shape != out[0].shape for x in out):
         raise ValueError("job tables differ in shape")
     return out
 
@@ -136,32 +137,46 @@ def simulate(arrival, prompt, output, *, policy: str, B: int, alpha: int, M_kv: 
     """
     p = make_params(policy, B, alpha, M_kv, cost_c, cost_tau, beta_sqrt17,
                     device=_is_torch(arrival), resume_fill=resume_fill)
-    if _is_torch(arrival):
+    return _simulate("fsched_simulate", p, (arrival, prompt, output), schedule, stream)
+
+
+def simulate_robust(arrival, prompt, output, upper, *, B: int, alpha: int, M_kv: int = 0,
+                    cost_c: int = 0, cost_tau: int = 1, beta_sqrt17: bool = False,
+                    resume_fill: bool = False, schedule: bool = False, stream=None):
+    """fsched_simulate_robust: Robust-ISJL planned on prompt + upper (upper >= output).
+
+    Same inputs and returns as ``simulate``; ``upper`` is shaped like the tables."""
+    p = make_params("isjl", B, alpha, M_kv, cost_c, cost_tau, beta_sqrt17,
+                    device=_is_torch(arrival), resume_fill=resume_fill)
+    return _simulate("fsched_simulate_robust", p, (arrival, prompt, output, upper), schedule,
+                     stream)
+
+
+def _simulate(name, p, tables, schedule, stream):
+    fn = getattr(lib(), name)
+    if _is_torch(tables[0]):
         import torch
-        a, pr, o = _torch_tables(arrival, prompt, output)
-        n_inst, n = a.shape
-        out = torch.empty((n_inst, 13), dtype=torch.int64, device=a.device)
-        st = torch.empty((n_inst, n), dtype=torch.int32, device=a.device) if schedule else None
-        fi = torch.empty((n_inst, n), dtype=torch.int32, device=a.device) if schedule else None
-        rc = lib().fsched_simulate(ctypes.byref(p), n_inst, n, a.data_ptr(), pr.data_ptr(),
-                                   o.data_ptr(), out.data_ptr(),
-                                   st.data_ptr() if st is not None else None,
-                                   fi.data_ptr() if fi is not None else None,
-                                   _stream_handle(torch, stream))
+        ts = _torch_tables(*tables)
+        n_inst, n = ts[0].shape
+        out = torch.empty((n_inst, 13), dtype=torch.int64, device=ts[0].device)
+        st = torch.empty((n_inst, n), dtype=torch.int32, device=ts[0].device) if schedule else None
+        fi = torch.empty((n_inst, n), dtype=torch.int32, device=ts[0].device) if schedule else None
+        rc = fn(ctypes.byref(p), n_inst, n, *[x.data_ptr() for x in ts], out.data_ptr(),
+                st.data_ptr() if st is not None else None,
+                fi.data_ptr() if fi is not None else None, _stream_handle(torch, stream))
         if rc:
-            raise FschedError(rc, "fsched_simulate")
+            raise FschedError(rc, name)
         return out, st, fi
-    a, pr, o = _np_tables(arrival, prompt, output)
-    n_inst, n = a.shape
+    ts = _np_tables(*tables)
+    n_inst, n = ts[0].shape
     out = np.zeros(n_inst, dtype=METRICS_DTYPE)
     st = np.empty((n_inst, n), np.int32) if schedule else None
     fi = np.empty((n_inst, n), np.int32) if schedule else None
-    rc = lib().fsched_simulate(ctypes.byref(p), n_inst, n, a.ctypes.data, pr.ctypes.data,
-                               o.ctypes.data, out.ctypes.data,
-                               st.ctypes.data if st is not None else None,
-                               fi.ctypes.data if fi is not None else None, None)
+    rc = fn(ctypes.byref(p), n_inst, n, *[x.ctypes.data for x in ts], out.ctypes.data,
+            st.ctypes.data if st is not None else None,
+            fi.ctypes.data if fi is not None else None, None)
     if rc:
-        raise FschedError(rc, "fsched_simulate")
+        raise FschedError(rc, name)
     return out, st, fi
 
 

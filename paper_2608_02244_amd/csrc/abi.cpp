@@ -89,7 +89,8 @@ struct Staging {
 
 int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int32_t* arrival,
                     const int32_t* prompt, const int32_t* output, fsched_metrics* out,
-                    int64_t* out_T, int32_t* start, int32_t* finish, hipStream_t s) {
+                    int64_t* out_T, int32_t* start, int32_t* finish, hipStream_t s,
+                    const int32_t* upper = nullptr) {
   const int Beff = (p->B == 0 || p->B > n) ? n : p->B;
   if (n > fs::MAX_JOBS || Beff > fs::MAX_WORKERS) return FSCHED_ETOOLARGE;
   int K = 1;
@@ -119,6 +120,7 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
   a.arrival = arrival;
   a.prompt = prompt;
   a.output = output;
+  a.upper = upper;
   a.out = out;
   a.out_T = out_T;
   a.start = start;
@@ -139,12 +141,58 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
     switch (p->policy) {
       case FSCHED_FCFS: e = fs::launch_sim_fcfs(b, K, NW, general, wpb, lds, s); break;
       case FSCHED_LJF: e = fs::launch_sim_ljf(b, K, NW, general, wpb, lds, s); break;
-      case FSCHED_ISJL: e = fs::launch_sim_isjl(b, K, NW, general, wpb, lds, s); break;
+      case FSCHED_ISJL:
+        e = upper ? fs::launch_sim_isjl_robust(b, K, NW, general, wpb, lds, s)
+                  : fs::launch_sim_isjl(b, K, NW, general, wpb, lds, s);
+        break;
       default: e = fs::launch_sim_sjf(b, K, NW, general, wpb, lds, s); break;
     }
     if (e != hipSuccess) return hip_fail(e);
   }
   return FSCHED_OK;
+}
+
+// fsched_simulate and fsched_simulate_robust (upper non-null).
+int simulate_entry(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
+                   const int32_t* arrival, const int32_t* prompt, const int32_t* output,
+                   const int32_t* upper, fsched_metrics* out, int32_t* start, int32_t* finish,
+                   void* stream) {
+  int rc = check_params(p, true);
+  if (rc) return rc;
+  if (n_inst < 0 || n_jobs < 1) return FSCHED_EINVAL;
+  if (n_inst == 0) return FSCHED_OK;
+  if (!arrival || !prompt || !output || !out) return FSCHED_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  if (p->flags & FSCHED_F_DEVICE_PTRS) {
+    rc = launch_simulate(p, n_inst, n_jobs, arrival, prompt, output, out, nullptr, start, finish,
+                         s, upper);
+    if (rc) return rc;
+    if (p->flags & FSCHED_F_SYNC) {
+      hipError_t e = hipStreamSynchronize(s);
+      if (e != hipSuccess) return hip_fail(e);
+    }
+    return FSCHED_OK;
+  }
+  const size_t cells = (size_t)n_inst * (size_t)n_jobs;
+  const size_t tb = cells * sizeof(int32_t);
+  Staging st;
+  const int32_t* da = (const int32_t*)st.upload(arrival, tb);
+  const int32_t* dp = (const int32_t*)st.upload(prompt, tb);
+  const int32_t* dq = (const int32_t*)st.upload(output, tb);
+  const int32_t* du = upper ? (const int32_t*)st.upload(upper, tb) : nullptr;
+  fsched_metrics* dout = (fsched_metrics*)st.alloc((size_t)n_inst * sizeof(fsched_metrics));
+  int32_t* dst = start ? (int32_t*)st.alloc(tb) : nullptr;
+  int32_t* dfi = finish ? (int32_t*)st.alloc(tb) : nullptr;
+  if (st.err != hipSuccess) return hip_fail(st.err);
+  rc = launch_simulate(p, n_inst, n_jobs, da, dp, dq, dout, nullptr, dst, dfi, s, du);
+  if (rc) return rc;
+  hipError_t e = hipStreamSynchronize(s);
+  if (e == hipSuccess)
+    e = hipMemcpy(out, dout, (size_t)n_inst * sizeof(fsched_metrics), hipMemcpyDeviceToHost);
+  if (e == hipSuccess && start) e = hipMemcpy(start, dst, tb, hipMemcpyDeviceToHost);
+  if (e == hipSuccess && finish) e = hipMemcpy(finish, dfi, tb, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e);
+  return markers_to_code(out, n_inst);
 }
 
 }  // namespace
@@ -172,41 +220,19 @@ int fsched_last_hip_error(void) { return g_last_hip; }
 int fsched_simulate(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
                     const int32_t* arrival, const int32_t* prompt, const int32_t* output,
                     fsched_metrics* out, int32_t* start, int32_t* finish, void* stream) {
-  int rc = check_params(p, true);
-  if (rc) return rc;
-  if (n_inst < 0 || n_jobs < 1) return FSCHED_EINVAL;
-  if (n_inst == 0) return FSCHED_OK;
-  if (!arrival || !prompt || !output || !out) return FSCHED_EINVAL;
-  hipStream_t s = (hipStream_t)stream;
-  if (p->flags & FSCHED_F_DEVICE_PTRS) {
-    rc = launch_simulate(p, n_inst, n_jobs, arrival, prompt, output, out, nullptr, start, finish,
-                         s);
-    if (rc) return rc;
-    if (p->flags & FSCHED_F_SYNC) {
-      hipError_t e = hipStreamSynchronize(s);
-      if (e != hipSuccess) return hip_fail(e);
-    }
-    return FSCHED_OK;
-  }
-  const size_t cells = (size_t)n_inst * (size_t)n_jobs;
-  const size_t tb = cells * sizeof(int32_t);
-  Staging st;
-  const int32_t* da = (const int32_t*)st.upload(arrival, tb);
-  const int32_t* dp = (const int32_t*)st.upload(prompt, tb);
-  const int32_t* dq = (const int32_t*)st.upload(output, tb);
-  fsched_metrics* dout = (fsched_metrics*)st.alloc((size_t)n_inst * sizeof(fsched_metrics));
-  int32_t* dst = start ? (int32_t*)st.alloc(tb) : nullptr;
-  int32_t* dfi = finish ? (int32_t*)st.alloc(tb) : nullptr;
-  if (st.err != hipSuccess) return hip_fail(st.err);
-  rc = launch_simulate(p, n_inst, n_jobs, da, dp, dq, dout, nullptr, dst, dfi, s);
-  if (rc) return rc;
-  hipError_t e = hipStreamSynchronize(s);
-  if (e == hipSuccess)
-    e = hipMemcpy(out, dout, (size_t)n_inst * sizeof(fsched_metrics), hipMemcpyDeviceToHost);
-  if (e == hipSuccess && start) e = hipMemcpy(start, dst, tb, hipMemcpyDeviceToHost);
-  if (e == hipSuccess && finish) e = hipMemcpy(finish, dfi, tb, hipMemcpyDeviceToHost);
-  if (e != hipSuccess) return hip_fail(e);
-  return markers_to_code(out, n_inst);
+  return simulate_entry(p, n_inst, n_jobs, arrival, prompt, output, nullptr, out, start, finish,
+                        stream);
+}
+
+int fsched_simulate_robust(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
+                           const int32_t* arrival, const int32_t* prompt, const int32_t* output,
+                           const int32_t* upper, fsched_metrics* out, int32_t* start,
+                           int32_t* finish, void* stream) {
+  if (!p) return FSCHED_EINVAL;
+  if (!upper) return FSCHED_EINVAL;
+  if (p->policy != FSCHED_ISJL) return FSCHED_ENOTIMPL;
+  return simulate_entry(p, n_inst, n_jobs, arrival, prompt, output, upper, out, start, finish,
+                        stream);
 }
 
 int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs,

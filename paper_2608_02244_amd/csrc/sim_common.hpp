@@ -35,6 +35,7 @@ struct SimArgs {
   const int32_t* arrival;
   const int32_t* prompt;
   const int32_t* output;
+  const int32_t* upper;  // predicted upper bounds of the outputs (Robust-ISJL), else null
   fsched_metrics* out;  // per-instance metrics, or
   int64_t* out_T;       // when non-null: only the makespan (or marker) per instance
   int32_t* start;
@@ -49,6 +50,9 @@ hipError_t launch_sim_ljf(const SimArgs& a, int K, int NW, bool general, int wav
                           size_t lds_bytes, hipStream_t s);
 hipError_t launch_sim_isjl(const SimArgs& a, int K, int NW, bool general, int waves_per_block,
                            size_t lds_bytes, hipStream_t s);
+// Robust-ISJL (Section 3.4): ISJL planning on prompt + upper[i].
+hipError_t launch_sim_isjl_robust(const SimArgs& a, int K, int NW, bool general,
+                                  int waves_per_block, size_t lds_bytes, hipStream_t s);
 hipError_t launch_sim_sjf(const SimArgs& a, int K, int NW, bool general, int waves_per_block,
                           size_t lds_bytes, hipStream_t s);
 

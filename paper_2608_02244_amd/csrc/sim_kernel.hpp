@@ -152,8 +152,12 @@ struct SimState {
   int64_t res, sum_s, sum_comp;
 };
 
-template <int POL, int K, int NW, bool GEN>
+// ROB: Robust-ISJL (Section 3.4): ordering, packs, caps and the KV reservation
+// use prompt + the predicted upper bound of the output; each job still runs its
+// true length, and fairness is checked on true progress.
+template <int POL, int K, int NW, bool GEN, bool ROB>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 : 1))) void simulate_kernel(SimArgs a) {
+  static_assert(!ROB || POL == POL_ISJL, "predicted sizes: ISJL only");
   extern __shared__ uint32_t lds_raw[];
   const int wib = threadIdx.x >> 6;
   const int64_t inst = (int64_t)blockIdx.x * (blockDim.x >> 6) + wib;
@@ -171,6 +175,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
   const int32_t* A = a.arrival + row;
   const int32_t* P = a.prompt + row;
   const int32_t* O = a.output + row;
+  const int32_t* U = ROB ? a.upper + row : nullptr;  // predicted upper bounds of the outputs
+  // true service length of job j (ROB: the length that plans used was larger)
+  auto true_len = [&](int j, int plan) -> int { return ROB ? P[j] + O[j] : plan; };
 
   if (GEN) {  // only instances the sorted-arrival kernel deferred
     const int64_t prev = a.out_T ? a.out_T[inst] : a.out[inst].T;
@@ -190,21 +197,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
     const int i = i0 + lane;
     const bool in = i < n;
     const int ar = in ? A[i] : 0x7FFFFFFF, p = in ? P[i] : 0, o = in ? O[i] : 1;
+    const int u = (ROB && in) ? U[i] : o;
     int prev = __shfl_up(ar, 1);
     if (lane == 0) prev = i0 > 0 ? carry_ar : ar;
     carry_ar = readlane(ar, WAVE - 1);
     uint32_t key = 0xFFFFFFFFu;
     if (in) {
-      bad |= (ar < 0) | (p < 0) | (o < 1);
+      bad |= (ar < 0) | (p < 0) | (o < 1) | (u < o);
       const int64_t len = (int64_t)p + (int64_t)o;
-      big |= (len >= LEN_LIMIT);
+      const int64_t plan_len = (int64_t)p + (int64_t)u;
+      big |= (plan_len >= LEN_LIMIT);
       unsorted |= (prev > ar);
       if (len < LEN_LIMIT && len > maxlen) maxlen = (int)len;
       if (ar > maxarr) maxarr = ar;
       osum += len;
       qsum += len * (len + 1) / 2;
       rsum += ar;
-      const uint32_t l32 = (uint32_t)len & LMASK;
+      const uint32_t l32 = (uint32_t)(ROB ? plan_len : len) & LMASK;
       if (POL == POL_LJF || POL == POL_ISJL) key = ((LMASK - l32) << 12) | (uint32_t)i;
       else if (POL == POL_SJF) key = (l32 << 12) | (uint32_t)i;
       else if (GEN) key = (((uint32_t)ar & LMASK) << 12) | (uint32_t)i;
@@ -284,10 +293,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
   const int alpha = a.alpha;
   const int64_t M = a.M;
   int ws_start[K], ws_end[K];
+  int ws_plan[K];  // ROB: planning size of the running job (its KV reservation)
   uint32_t ws_q[K];
   bool valid[K];
 #pragma unroll
   for (int k = 0; k < K; ++k) {
+    ws_plan[k] = 0;
     ws_start[k] = IDLE;
     ws_end[k] = IDLE;
     ws_q[k] = QNONE | (QNONE << 16);
@@ -347,7 +358,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
     } else if (j < n) {
       // rank of job j: position of its priority key in W (binary search)
       rel_t = A[j];
-      uint32_t len = (uint32_t)(P[j] + O[j]);
+      uint32_t len = (uint32_t)(P[j] + (ROB ? U[j] : O[j]));
       uint32_t key;
       if (POL == POL_SJF) key = (len << 12) | (uint32_t)j;
       else key = ((LMASK - len) << 12) | (uint32_t)j;
@@ -418,7 +429,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       tot64 = run - S.res;
     }
     if (na == 0) return 0;
-    int base = 0, lsum = 0;
+    int base = 0, lsum = 0, lplan = 0, lmin = IDLE;
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       if (base < na) {
@@ -428,24 +439,37 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
         const int idx = base + mbcnt(bm);
         if (el && idx < na) {
           const uint32_t wv = W[STG[idx]];
-          const int len = plen(wv);
+          const int plan = plen(wv);
+          const int len = true_len(pid(wv), plan);
           ws_start[k] = t;
           ws_end[k] = t + len;
           emit(pid(wv), t, len);
           lsum += len;
+          if (ROB) {
+            ws_plan[k] = plan;
+            lplan += plan;
+            lmin = min(lmin, len);
+          }
         }
         base += __builtin_popcountll(bm);
       }
     }
-    const int tot = tot64 >= 0 ? (int)tot64 : wave_sum(lsum);
-    // the gathered jobs are in priority order, so the shortest admitted one is
-    // the last (longest first) or the first (SJF)
-    adm_minlen = min(adm_minlen, plen(W[STG[POL == POL_SJF ? 0 : na - 1]]));
+    int tot, ptot;  // true and planned lengths admitted
+    if (ROB) {
+      tot = wave_sum(lsum);
+      ptot = tot64 >= 0 ? (int)tot64 : wave_sum(lplan);
+      adm_minlen = min(adm_minlen, wave_min(lmin));
+    } else {
+      tot = ptot = tot64 >= 0 ? (int)tot64 : wave_sum(lsum);
+      // the gathered jobs are in priority order, so the shortest admitted one
+      // is the last (longest first) or the first (SJF)
+      adm_minlen = min(adm_minlen, plen(W[STG[POL == POL_SJF ? 0 : na - 1]]));
+    }
     pool.clear_upto(STG[na - 1], lane);  // the first na queued ranks
     qcount -= na;
     adm += na;
     adm_len += tot;
-    S.res += tot;
+    S.res += ptot;
     S.nact += na;
     return na;
   };
@@ -456,7 +480,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
     if (S.min_end == t) {
       // the earliest / latest start is searched again only if a job holding
       // it retires
-      int nret = 0, lsum = 0, me = IDLE;
+      int nret = 0, lsum = 0, lplan = 0, me = IDLE;
       bool hmin = false, hmax = false;
 #pragma unroll
       for (int k = 0; k < K; ++k) {
@@ -464,6 +488,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
         nret += __builtin_popcountll(ballot(r));
         if (r) {
           lsum += ws_end[k] - ws_start[k];
+          if (ROB) lplan += ws_plan[k];
           hmin |= ws_start[k] == S.min_s;
           hmax |= ws_start[k] == S.max_s;
           ws_end[k] = IDLE;
@@ -488,7 +513,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       }
       S.ndone += nret;
       S.nact -= nret;
-      S.res -= lret;
+      S.res -= ROB ? wave_sum(lplan) : lret;
       S.sum_s -= (int64_t)nret * t - (int64_t)lret;
     }
     if (S.ndone == n) break;
@@ -828,15 +853,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
             tot = (int)(rres - S.res);
             ncand = nk;
           }
-          int mlen = IDLE;
+          int mlen = IDLE, ltrue = 0;
 #pragma unroll
           for (int k = 0; k < K; ++k) {
             if (cand[k]) {
               uint32_t h = ws_q[k] & 0xFFFFu;
               uint32_t wv = W[h];
-              int len = plen(wv);
+              const int plan = plen(wv);
+              const int len = true_len(pid(wv), plan);
               ws_start[k] = t;
               ws_end[k] = t + len;
+              if (ROB) {
+                ws_plan[k] = plan;
+                ltrue += len;
+              }
               mlen = min(mlen, len);
               emit(pid(wv), t, len);
               uint32_t nx = QN[h];
@@ -845,7 +875,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
           }
           adm_minlen = min(adm_minlen, wave_min(mlen));
           adm += ncand;
-          adm_len += tot;
+          adm_len += ROB ? wave_sum(ltrue) : tot;
           S.res += tot;
           S.nact += ncand;
           planned -= ncand;
@@ -1114,7 +1144,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       for (int k = 0; k < K; ++k) {
         if (ws_end[k] <= tau_end) {
           rc++;
-          rl += ws_end[k] - ws_start[k];
+          rl += ROB ? ws_plan[k] : ws_end[k] - ws_start[k];
           ws_end[k] = IDLE;
           ws_start[k] = IDLE;
         }
@@ -1224,14 +1254,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
   }
 }
 
-template <int POL>
+template <int POL, bool ROB = false>
 hipError_t launch_sim(const SimArgs& a, int K, int NW, bool general, int wpb, size_t lds,
                       hipStream_t s) {
   const int64_t blocks = (a.n_inst + wpb - 1) / wpb;
   dim3 grid((unsigned)blocks), block((unsigned)(wpb * WAVE));
 #define FS_LAUNCH(KK, NN, GG)                                                        \
   if (K == KK && NW == NN && general == GG) {                                        \
-    hipLaunchKernelGGL((simulate_kernel<POL, KK, NN, GG>), grid, block, lds, s, a);  \
+    hipLaunchKernelGGL((simulate_kernel<POL, KK, NN, GG, ROB>), grid, block, lds, s, a);  \
     return hipGetLastError();                                                        \
   }
 #define FS_LAUNCH_K(KK) \

@@ -1,4 +1,4 @@
-"""The Robust-ISJL experiment (Section 3.5): ISJL planned on the upper ends u_i of
+"""The Robust-ISJL experiment (Section 3.4): ISJL planned on the upper ends u_i of
 output-length prediction intervals, run on the true lengths.
 
 On tiny offline instances (all releases at 0, no KV budget) it checks, per
@@ -82,11 +82,17 @@ def delta_pack(length, slack, alpha: int, B: int, chunk: int = 4096) -> np.ndarr
 
 
 def gpu_quad(a, p, o, u, B: int, alpha: int, M_kv: int = 0):
-    """Through the HIP library (host buffers): T_R, its unfair steps, T_OPT,
-    T_ISJL(I) and T_ISJL(I_u) per instance."""
+    """Through the HIP library on cuda:0: T_R, its unfair steps, T_OPT,
+    T_ISJL(I) and T_ISJL(I_u) per instance.  T_OPT is negative (a marker) for an
+    instance whose exhaustive search gave up (its push limit)."""
+    import torch
     from . import bruteforce_opt, simulate, simulate_robust
     mr, _, _ = simulate_robust(a, p, o, u, B=B, alpha=alpha, M_kv=M_kv, cost_c=0, cost_tau=0)
-    T_opt, _ = bruteforce_opt(a, p, o, B=B, alpha=alpha, M_kv=M_kv)
+    dev = torch.device("cuda:0")
+    ta, tp, to = (torch.from_numpy(np.ascontiguousarray(x, dtype=np.int32)).to(dev)
+                  for x in (a, p, o))
+    T_opt, _ = bruteforce_opt(ta, tp, to, B=B, alpha=alpha, M_kv=M_kv)
+    T_opt = T_opt.cpu().numpy()
     mi, _, _ = simulate(a, p, o, policy="isjl", B=B, alpha=alpha, M_kv=M_kv, cost_c=0,
                         cost_tau=0)
     mu, _, _ = simulate(a, p, u, policy="isjl", B=B, alpha=alpha, M_kv=M_kv, cost_c=0,
@@ -98,7 +104,8 @@ def gpu_quad(a, p, o, u, B: int, alpha: int, M_kv: int = 0):
 def run(quad: Callable, a, p, o, u, alphas: Sequence[int], B: int = 2) -> Dict:
     """Per alpha: instances, fairness violations, violations of the guarantee,
     of the corollary and of the proof's first step (with the worst instance of
-    each), the smallest T_OPT / T_R and the mean T_R / T_ISJL."""
+    each), the smallest T_OPT / T_R and the mean T_R / T_ISJL.  Instances whose
+    optimum was not found (negative T_OPT) are left out and counted."""
     P = np.asarray(p, np.int64)
     O = np.asarray(o, np.int64)
     U = np.asarray(u, np.int64)
@@ -112,9 +119,12 @@ def run(quad: Callable, a, p, o, u, alphas: Sequence[int], B: int = 2) -> Dict:
     rows: List[Dict] = []
     for al in alphas:
         T_r, unfair, T_opt, T_i, T_u = (np.asarray(x, np.int64) for x in quad(a, p, o, u, B, al))
+        if (T_r < 0).any() or (T_i < 0).any() or (T_u < 0).any():
+            raise RuntimeError("an instance reported an error marker")
+        solved = T_opt >= 0
         dp = delta_pack(length, slack, al, B)
-        thm = 3 * T_r > 4 * (T_opt + dp)
-        cor = 4 * T_opt * (tot_len + Bc * tot_slack) < 3 * T_r * tot_len
+        thm = solved & (3 * T_r > 4 * (T_opt + dp))
+        cor = solved & (4 * T_opt * (tot_len + Bc * tot_slack) < 3 * T_r * tot_len)
         step1 = T_r > T_u
 
         def worst(mask, gap):
@@ -127,14 +137,14 @@ def run(quad: Callable, a, p, o, u, alphas: Sequence[int], B: int = 2) -> Dict:
                     "lengths": length[j].tolist(), "slack": slack[j].tolist()}
 
         rows.append({
-            "alpha": int(al), "n": int(len(T_r)),
+            "alpha": int(al), "n": int(len(T_r)), "opt_unsolved": int((~solved).sum()),
             "unfair": int((unfair > 0).sum()),
             "thm_violations": int(thm.sum()),
             "thm_worst": worst(thm, (3 * T_r - 4 * (T_opt + dp)) / np.maximum(T_r, 1)),
             "cor_violations": int(cor.sum()),
             "step1_violations": int(step1.sum()),
             "step1_worst": worst(step1, (T_r - T_u) / np.maximum(T_u, 1)),
-            "min_opt_over_r": float((T_opt / T_r).min()),
+            "min_opt_over_r": float((T_opt[solved] / T_r[solved]).min()),
             "mean_r_over_isjl": float((T_r / T_i).mean()),
             "mean_delta_pack": float(dp.mean()), "mean_delta": float(tot_slack.mean()),
         })

@@ -1,4 +1,4 @@
-"""Robust-ISJL (Section 3.5) in the oracle, and the experiment driver on the CPU.
+"""Robust-ISJL (Section 3.4) in the oracle, and the experiment driver on the CPU.
 
 Pins: hand-traced examples (tests/golden/robust_examples.json), exact
 predictions reduce to ISJL, the fairness theorem (any upper bounds), the
