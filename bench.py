@@ -84,14 +84,15 @@ def main() -> int:
                     help="skip the per-alpha roofline lines of the fairness-budget sweep workload")
     ap.add_argument("--mode", default="simulate",
                     choices=["simulate", "copy", "decompose", "opt", "host", "profit",
-                             "gamma", "robust"],
+                             "gamma", "robust", "efficiency"],
                     help="simulate: the benchmark line; copy: a plain device copy of known size "
                          "(calibrates the HBM byte counters); decompose / opt: time the other "
                          "two library calls (for profiles); host: host-buffer calls, "
                          "PCIe copies included; profit: the linear-pricing experiment; "
                          "gamma: the competitive-ratio experiment; robust: Robust-ISJL on "
                          "predicted sizes (headline workload and the guarantee on tiny "
-                         "instances)")
+                         "instances); efficiency: throughput and AEL of every policy on the "
+                         "LMSYS-shaped workload")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the instances are "
@@ -118,6 +119,8 @@ def main() -> int:
         return time_gamma(args)
     if args.mode == "robust":
         return time_robust(torch, np, workload, fs, args)
+    if args.mode == "efficiency":
+        return time_efficiency(np, workload)
     w = workload.WORKLOADS[args.workload]
     alpha = w.alphas[0]
     policy = "isjl"
@@ -353,6 +356,25 @@ def time_robust(torch, np, workload, fs, args) -> int:
                       f"{rows[-1]['seconds']:.1f} s", file=sys.stderr, flush=True)
             tiny.append({"B": B, "instances": n, "slack": slack, "rows": rows})
     out["tiny"] = {"workload": "tiny_opt_1048576x8", "runs": tiny}
+    print(json.dumps(out))
+    return 0
+
+
+def time_efficiency(np, workload) -> int:
+    """Throughput and AEL of FCFS, SJF, LJF, ISJL(50/100/150) at B = 16 and 32 on
+    the 256 instances of the LMSYS-shaped workload, with its Poisson releases and
+    with every request released at step 0."""
+    from paper_2608_02244_amd import efficiency as ef
+    a, p, o = workload.generate("lmsys_shaped_256x2000")
+    out = {"mode": "efficiency", "workload": "lmsys_shaped_256x2000"}
+    ef.run_table(ef.gpu_simulate, a[:8], p[:8], o[:8], Bs=(16,))  # warm-up
+    for name, arr in (("poisson", a), ("offline", np.zeros_like(a))):
+        t0 = time.perf_counter()
+        tab = ef.run_table(ef.gpu_simulate, arr, p, o)
+        out[name] = {"seconds": time.perf_counter() - t0, "table": {str(B): r for B, r in
+                                                                    tab.items()},
+                     "markdown": ef.format_table(tab)}
+        print(f"efficiency {name}: {out[name]['seconds']:.2f} s", file=sys.stderr, flush=True)
     print(json.dumps(out))
     return 0
 

@@ -115,6 +115,16 @@ WORKLOADS: Dict[str, Workload] = {w.name: w for w in [
              B=2, M_kv=16, alphas=(1, 2, 4), cost_c=0, cost_tau=1,
              policies=("isjl",), note="exact optimum by exhaustive search; "
              "also evaluated with no KV budget"),
+    # Shaped like the conversation sample of the paper's system-efficiency
+    # section (2,000 requests; total tokens with mean 126, median 90, max 905):
+    # total tokens LN(median 90, sigma 0.82) clipped to 1..905 (mean 126), all in
+    # the output column; Poisson arrivals at 0.25 requests per step (twice the
+    # service rate of B = 16 at the mean length).  A synthetic stand-in, not the
+    # dataset.
+    Workload("lmsys_shaped_256x2000", 6, 256, 2000, 0.25, uniform(0, 0),
+             lognormal(90.0, 0.82, 1, 905), B=16, M_kv=0, alphas=(50, 100, 150),
+             cost_c=0, cost_tau=1, policies=("fcfs", "sjf", "ljf", "isjl"),
+             note="system-efficiency table shape; B = 16 and 32"),
 ]}
 
 WORKLOAD_ORDER: List[str] = list(WORKLOADS)
