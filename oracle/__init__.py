@@ -24,6 +24,7 @@ ALPHA_INF = 2**31 - 1
 POLICIES = {"fcfs": 0, "ljf": 1, "isjl": 2, "sjf": 3}
 FLAG_BETA_SQRT17 = 8
 FLAG_RESUME_FILL = 16
+FLAG_PREFILL = 32  # prompt prefilled at admission: service = output, footprint prompt + progress
 
 METRIC_FIELDS = ["T", "O", "Q", "E", "C", "W", "sum_completion", "sum_latency",
                  "sum_extent", "busy_steps", "peak_kv", "unfair_steps",

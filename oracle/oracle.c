@@ -48,6 +48,7 @@
 
 #define FLAG_BETA_SQRT17 8u
 #define FLAG_RESUME_FILL 16u
+#define FLAG_PREFILL 32u
 
 #define ALPHA_INF_SENTINEL 2147483647
 
@@ -70,6 +71,10 @@ typedef struct {
   int64_t* len;       /* service length = prompt + output         */
   int64_t* plan;      /* planning size: len, or prompt + the predicted upper
                          bound of the output (Robust-ISJL, Section 3.4) */
+  int64_t* resv;      /* KV reservation while active: plan, or prompt + plan in
+                         the prefill-at-admission variant */
+  int64_t* pre;       /* footprint offset: NULL (chunked prompt), or the prompt
+                         when it is prefilled at admission */
 } or_inst;
 
 /* ------------------------------------------------------------------ */
@@ -89,17 +94,21 @@ static void account_step(or_acc* a, const or_inst* I, int64_t t, const int64_t* 
     a->W += I->c;
     return;
   }
-  int64_t mx = INT64_MIN, mn = INT64_MAX, sr = 0;
+  /* footprint r = progress (+ the prompt when it was prefilled at admission);
+   * the fairness range is over progress (eq. (1)) */
+  int64_t mx = INT64_MIN, sr = 0, amx = INT64_MIN, amn = INT64_MAX;
   for (int32_t k = 0; k < nact; ++k) {
-    int64_t r = t - start[act[k]] + 1;
+    int64_t a_k = t - start[act[k]] + 1;
+    int64_t r = a_k + (I->pre ? I->pre[act[k]] : 0);
     if (r > mx) mx = r;
-    if (r < mn) mn = r;
     sr += r;
+    if (a_k > amx) amx = a_k;
+    if (a_k < amn) amn = a_k;
   }
   a->E += (int64_t)nact * mx - sr;
   a->C += I->c + I->tau * (int64_t)nact * mx;
   a->W += I->c + I->tau * mx;
-  int64_t ext = mx - mn;
+  int64_t ext = amx - amn;
   a->sum_extent += ext;
   a->busy += 1;
   if (ext > I->alpha) a->unfair += 1;
@@ -113,9 +122,11 @@ static void finish_metrics(or_metrics* m, const or_inst* I, const or_acc* a, int
   memset(m, 0, sizeof(*m));
   int64_t O = 0, Q = 0, sc = 0, sl = 0;
   for (int32_t i = 0; i < I->n; ++i) {
-    int64_t l = I->len[i];
-    O += l;
-    Q += l * (l + 1) / 2; /* Q = sum_i sum_{k=1..l_i} k, Theorem 5.1 */
+    int64_t l = I->len[i], q = I->pre ? I->pre[i] : 0;
+    O += q + l; /* tokens served */
+    /* Q = sum_i of the footprint summed over the job's own steps, Theorem 5.1:
+     * sum_{k=1..l_i} (q_i + k) */
+    Q += l * q + l * (l + 1) / 2;
     sc += start[i] + l;
     sl += start[i] + l - I->arrival[i];
   }
@@ -195,14 +206,14 @@ typedef struct {
  * a job that would run alone is always admissible). */
 static int kv_ok(const or_sim* S, int32_t j) {
   if (S->I->M == 0 || S->nact == 0) return 1;
-  return S->res + S->I->plan[j] <= S->I->M;
+  return S->res + S->I->resv[j] <= S->I->M;
 }
 
 static void admit(or_sim* S, int32_t j, int64_t t) {
   S->st[j] = ST_ACTIVE;
   S->start[j] = t;
   S->act[S->nact++] = j;
-  S->res += S->I->plan[j];
+  S->res += S->I->resv[j];
 }
 
 static int released(const or_inst* I, int32_t j, int64_t t) { return I->arrival[j] <= t; }
@@ -434,6 +445,8 @@ static int make_inst(or_inst* I, int32_t n, const int32_t* arrival, const int32_
   if (!I->len) return OR_ENOMEM;
   for (int32_t i = 0; i < n; ++i) I->len[i] = (int64_t)prompt[i] + output[i];
   I->plan = I->len;
+  I->resv = I->len;
+  I->pre = NULL;
   return OR_OK;
 }
 
@@ -452,23 +465,43 @@ static int simulate_impl(int32_t n, const int32_t* arrival, const int32_t* promp
   or_inst I;
   int rc = make_inst(&I, n, arrival, prompt, output, B, alpha, M_kv, cost_c, cost_tau);
   if (rc) return rc;
-  if (upper) {
-    /* Robust-ISJL (Section 3.4): sizes used for ordering, packing, M, the caps
-     * and (reading) the KV reservation are prompt + the predicted upper bound
-     * of the output; jobs still run their true length. */
-    I.plan = (int64_t*)malloc(sizeof(int64_t) * (size_t)n);
-    if (!I.plan) {
+  int64_t* extra = NULL; /* plan, resv and pre of the variants */
+  const int prefill = (flags & FLAG_PREFILL) != 0;
+  if (upper || prefill) {
+    extra = (int64_t*)malloc(sizeof(int64_t) * 3 * (size_t)n);
+    if (!extra) {
       free(I.len);
       return OR_ENOMEM;
     }
+    I.plan = extra;
+    I.resv = extra + n;
     for (int32_t i = 0; i < n; ++i) {
-      if (upper[i] < output[i] || (int64_t)prompt[i] + upper[i] > (1 << 30)) {
+      if (upper && (upper[i] < output[i] || (int64_t)prompt[i] + upper[i] > (1 << 30))) {
         const int code = upper[i] < output[i] ? OR_EINVAL : OR_ERANGE;
-        free(I.plan);
+        free(extra);
         free(I.len);
         return code;
       }
-      I.plan[i] = (int64_t)prompt[i] + upper[i];
+      /* Robust-ISJL (Section 3.4): the sizes used for ordering, packing, M, the
+       * caps and (reading) the KV reservation take the predicted upper bound of
+       * the output; jobs still run their true length. */
+      const int64_t out_plan = upper ? upper[i] : output[i];
+      if (prefill) {
+        /* Prefill at admission (reading of Section 1 with eq. (1)'s decode
+         * progress): the prompt is processed when the job is admitted, the job
+         * then runs one step per output token, its footprint is prompt +
+         * progress, and it reserves prompt + output. */
+        I.len[i] = output[i];
+        I.plan[i] = out_plan;
+        I.resv[i] = (int64_t)prompt[i] + out_plan;
+      } else {
+        I.plan[i] = (int64_t)prompt[i] + out_plan;
+        I.resv[i] = I.plan[i];
+      }
+    }
+    if (prefill) {
+      I.pre = extra + 2 * (size_t)n;
+      for (int32_t i = 0; i < n; ++i) I.pre[i] = prompt[i];
     }
   }
   size_t nn = (size_t)n, nb = (size_t)I.B;
@@ -527,7 +560,7 @@ static int simulate_impl(int32_t n, const int32_t* arrival, const int32_t* promp
       int32_t j = S.act[k];
       if (S.start[j] + I.len[j] == t) {
         S.st[j] = ST_DONE;
-        S.res -= I.plan[j];
+        S.res -= I.resv[j];
         ndone++;
         if (policy == POL_ISJL) S.cur[S.wk[j]] = -1;
       } else {
@@ -580,7 +613,7 @@ done:
   free(S.qnext);
   free(S.planned);
   free(S.pool);
-  if (I.plan != I.len) free(I.plan);
+  free(extra);
   free(I.len);
   return rc;
 }
