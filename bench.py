@@ -84,7 +84,7 @@ def main() -> int:
                     help="skip the per-alpha roofline lines of the fairness-budget sweep workload")
     ap.add_argument("--mode", default="simulate",
                     choices=["simulate", "copy", "decompose", "opt", "host", "profit",
-                             "gamma", "robust", "efficiency"],
+                             "gamma", "robust", "efficiency", "prefill"],
                     help="simulate: the benchmark line; copy: a plain device copy of known size "
                          "(calibrates the HBM byte counters); decompose / opt: time the other "
                          "two library calls (for profiles); host: host-buffer calls, "
@@ -92,7 +92,8 @@ def main() -> int:
                          "gamma: the competitive-ratio experiment; robust: Robust-ISJL on "
                          "predicted sizes (headline workload and the guarantee on tiny "
                          "instances); efficiency: throughput and AEL of every policy on the "
-                         "LMSYS-shaped workload")
+                         "LMSYS-shaped workload; prefill: the prefill-at-admission variant "
+                         "of every policy on the headline workload")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the instances are "
@@ -121,6 +122,8 @@ def main() -> int:
         return time_robust(torch, np, workload, fs, args)
     if args.mode == "efficiency":
         return time_efficiency(np, workload)
+    if args.mode == "prefill":
+        return time_prefill(torch, np, workload, fs, args)
     w = workload.WORKLOADS[args.workload]
     alpha = w.alphas[0]
     policy = "isjl"
@@ -376,6 +379,46 @@ def time_efficiency(np, workload) -> int:
                      "markdown": ef.format_table(tab)}
         print(f"efficiency {name}: {out[name]['seconds']:.2f} s", file=sys.stderr, flush=True)
     print(json.dumps(out))
+    return 0
+
+
+def time_prefill(torch, np, workload, fs, args) -> int:
+    """Every policy in the prefill-at-admission variant on the headline workload
+    (the prompt is processed at admission, a job runs its output tokens), timed
+    with HIP events, beside ISJL in the chunked reading."""
+    w = workload.WORKLOADS[args.workload]
+    alpha = w.alphas[0]
+    dev = torch.device("cuda:0")
+    a, p, o = workload.generate(w)
+    ta, tp, to = (torch.from_numpy(x).to(dev) for x in (a, p, o))
+    stream = torch.cuda.current_stream()
+    rows = []
+    for pol, pre in (("isjl", False), ("isjl", True), ("ljf", True), ("fcfs", True),
+                     ("sjf", True)):
+        kw = dict(policy=pol, B=w.B, alpha=alpha if pol in ("isjl", "ljf") else fs.ALPHA_INF,
+                  M_kv=w.M_kv, cost_c=w.cost_c, cost_tau=w.cost_tau, prefill=pre)
+        m = fs.metrics_view(fs.simulate(ta, tp, to, **kw)[0])
+        if (m["T"] < 0).any():
+            raise RuntimeError("some instance reported an error marker")
+        for _ in range(args.warmup):
+            fs.simulate(ta, tp, to, **kw)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            fs.simulate(ta, tp, to, **kw)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        print(f"prefill={pre} {pol}: {ms:.2f} ms", file=sys.stderr, flush=True)
+        rows.append({"policy": pol, "prefill": pre, "ms_per_launch": ms,
+                     "instance_steps_per_s": float(m["T"].sum()) / (ms / 1e3),
+                     "mean_T": float(m["T"].mean()),
+                     "tokens_per_step": float(m["O"].sum() / m["T"].sum()),
+                     "mean_latency": float(m["sum_latency"].sum() / m["T"].size / w.n_jobs),
+                     "W_over_T": float(m["W"].sum() / m["T"].sum()),
+                     "unfair_steps": int(m["unfair_steps"].sum())})
+    print(json.dumps({"mode": "prefill", "workload": w.name, "alpha": alpha, "rows": rows}))
     return 0
 
 

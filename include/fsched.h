@@ -83,11 +83,24 @@ enum {
   FSCHED_F_BETA_SQRT17 = 8u, /* ISJL: beta = floor((sqrt(17)-1) alpha / 4), the
                                 B = 2 choice of Section 3.2; default beta = alpha
                                 (Section 3.3)                                   */
-  FSCHED_F_RESUME_FILL = 16u /* ISJL, experiments only: after Phase TWO stops on
+  FSCHED_F_RESUME_FILL = 16u, /* ISJL, experiments only: after Phase TWO stops on
                                 A_max > alpha, it resumes as soon as A_max <= alpha
                                 again instead of waiting for the machine to empty
                                 (the other reading of "repeat from Phase ONE"
                                 with busy workers, Algorithms 2 and 3)          */
+  FSCHED_F_PREFILL = 32u     /* simulate / simulate_robust: the prompt is
+                                prefilled when the job is admitted (Section 1's
+                                prefill pass; eq. (1)'s progress counts decode
+                                tokens): a job runs output_i steps, reserves
+                                prompt_i + output_i of M_kv, its footprint in the
+                                Section 5 batch cost is prompt_i + progress, and
+                                fairness, extent and A_max stay on progress.
+                                O counts prompt + output tokens; Q is the
+                                footprint summed over the job's own steps.
+                                Default: the chunked reading of Section 2 (a job
+                                runs prompt_i + output_i steps, footprint =
+                                progress).  The other calls return ENOTIMPL
+                                with it.                                        */
 };
 
 /* Scheduling and cost parameters (40 bytes, no padding). */
@@ -187,7 +200,8 @@ int fsched_simulate_robust(const fsched_params* p, int64_t n_inst, int32_t n_job
  *              2 more than B jobs active at some step; 4 reservations above
  *              M_kv with two or more jobs active; 8 progress range above alpha
  *              (eq. (1)); 16 a negative start (metrics are zero then).
- * p->policy and p->flags other than DEVICE_PTRS / SYNC are ignored.
+ * p->policy and p->flags other than DEVICE_PTRS / SYNC are ignored, except
+ * FSCHED_F_PREFILL (ENOTIMPL: schedules are scored in the chunked reading).
  * Errors as fsched_simulate. */
 int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
                           const int32_t* arrival, const int32_t* prompt,
@@ -206,7 +220,7 @@ int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs
  *   T_opt      [n_inst] int64 optimum makespan.
  *   start_opt  nullable [n_inst][n_jobs] int32: one optimal schedule.
  * p->policy, p->flags other than DEVICE_PTRS / SYNC, cost_c and cost_tau are
- * ignored. */
+ * ignored, except FSCHED_F_PREFILL (ENOTIMPL). */
 int fsched_bruteforce_opt(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
                           const int32_t* arrival, const int32_t* prompt, const int32_t* output,
                           int64_t* T_opt, int32_t* start_opt, void* stream);

@@ -302,7 +302,7 @@ static void phase_one(or_sim* S, const int32_t* ord_long, int64_t t, uint32_t fl
    * ISJL identical to LJF. */
   int64_t Bp = 0, resv = 0;
   for (int32_t q = 0; q < k && Bp < I->B; ++q) {
-    int64_t L = I->plan[S->pool[q]];
+    int64_t L = I->resv[S->pool[q]];
     if (I->M != 0 && q > 0 && resv + L > I->M) break;
     resv += L;
     Bp++;

@@ -23,7 +23,7 @@ LIB_PATH = os.path.join(_HERE, "libfsched.so")
 ALPHA_INF = 2**31 - 1
 UNLIMITED = 0
 POLICIES = {"fcfs": 0, "ljf": 1, "isjl": 2, "sjf": 3}
-F_DEVICE_PTRS, F_SYNC, F_BETA_SQRT17, F_RESUME_FILL = 1, 4, 8, 16
+F_DEVICE_PTRS, F_SYNC, F_BETA_SQRT17, F_RESUME_FILL, F_PREFILL = 1, 4, 8, 16, 32
 
 OK, EINVAL, ERANGE, ENOMEM, EDEVICE, ETOOLARGE, ENOTIMPL, EINTERNAL = 0, -1, -2, -3, -4, -5, -6, -7
 T_INVALID, T_RANGE, T_TOOLARGE, T_INTERNAL = -1, -2, -5, -7
@@ -80,9 +80,10 @@ def lib():
 
 def make_params(policy: str = "isjl", B: int = 0, alpha: int = ALPHA_INF, M_kv: int = 0,
                 cost_c: int = 0, cost_tau: int = 1, beta_sqrt17: bool = False,
-                device: bool = False, resume_fill: bool = False) -> Params:
+                device: bool = False, resume_fill: bool = False,
+                prefill: bool = False) -> Params:
     flags = (F_DEVICE_PTRS if device else 0) | (F_BETA_SQRT17 if beta_sqrt17 else 0) | \
-        (F_RESUME_FILL if resume_fill else 0)
+        (F_RESUME_FILL if resume_fill else 0) | (F_PREFILL if prefill else 0)
     return Params(B=B, alpha=alpha, M_kv=M_kv, policy=POLICIES[policy], flags=flags,
                   cost_c=cost_c, cost_tau=cost_tau)
 
@@ -128,26 +129,29 @@ def _stream_handle(torch, stream):
 
 def simulate(arrival, prompt, output, *, policy: str, B: int, alpha: int, M_kv: int = 0,
              cost_c: int = 0, cost_tau: int = 1, beta_sqrt17: bool = False,
-             resume_fill: bool = False, schedule: bool = False, stream=None):
-    """fsched_simulate over every row (instance) of the job tables.
+             resume_fill: bool = False, prefill: bool = False, schedule: bool = False,
+             stream=None):
+    """fsched_simulate over every row (instance) of the job tables (``prefill``:
+    the prompt is prefilled at admission, FSCHED_F_PREFILL).
 
     Torch inputs: returns (metrics [n_inst, 13] int64 tensor, start, finish) with
     start/finish None unless ``schedule``; nothing is synchronised.
     Numpy inputs: returns (metrics structured array, start, finish) in host memory.
     """
     p = make_params(policy, B, alpha, M_kv, cost_c, cost_tau, beta_sqrt17,
-                    device=_is_torch(arrival), resume_fill=resume_fill)
+                    device=_is_torch(arrival), resume_fill=resume_fill, prefill=prefill)
     return _simulate("fsched_simulate", p, (arrival, prompt, output), schedule, stream)
 
 
 def simulate_robust(arrival, prompt, output, upper, *, B: int, alpha: int, M_kv: int = 0,
                     cost_c: int = 0, cost_tau: int = 1, beta_sqrt17: bool = False,
-                    resume_fill: bool = False, schedule: bool = False, stream=None):
+                    resume_fill: bool = False, prefill: bool = False, schedule: bool = False,
+                    stream=None):
     """fsched_simulate_robust: Robust-ISJL planned on prompt + upper (upper >= output).
 
     Same inputs and returns as ``simulate``; ``upper`` is shaped like the tables."""
     p = make_params("isjl", B, alpha, M_kv, cost_c, cost_tau, beta_sqrt17,
-                    device=_is_torch(arrival), resume_fill=resume_fill)
+                    device=_is_torch(arrival), resume_fill=resume_fill, prefill=prefill)
     return _simulate("fsched_simulate_robust", p, (arrival, prompt, output, upper), schedule,
                      stream)
 

@@ -40,7 +40,8 @@ int check_params(const fsched_params* p, bool need_policy) {
     return FSCHED_EINVAL;
   if (need_policy && (p->policy < FSCHED_FCFS || p->policy > FSCHED_SJF)) return FSCHED_EINVAL;
   const uint32_t known =
-      FSCHED_F_DEVICE_PTRS | FSCHED_F_SYNC | FSCHED_F_BETA_SQRT17 | FSCHED_F_RESUME_FILL;
+      FSCHED_F_DEVICE_PTRS | FSCHED_F_SYNC | FSCHED_F_BETA_SQRT17 | FSCHED_F_RESUME_FILL |
+      FSCHED_F_PREFILL;
   if (p->flags & ~known) return FSCHED_EINVAL;
   return FSCHED_OK;
 }
@@ -138,14 +139,28 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
     while (wpb > 1 && per_wave * wpb > 64 * 1024) wpb >>= 1;
     size_t lds = per_wave * wpb;
     hipError_t e;
+    const bool pre = (p->flags & FSCHED_F_PREFILL) != 0;
     switch (p->policy) {
-      case FSCHED_FCFS: e = fs::launch_sim_fcfs(b, K, NW, general, wpb, lds, s); break;
-      case FSCHED_LJF: e = fs::launch_sim_ljf(b, K, NW, general, wpb, lds, s); break;
+      case FSCHED_FCFS:
+        e = pre ? fs::launch_sim_fcfs_prefill(b, K, NW, general, wpb, lds, s)
+                : fs::launch_sim_fcfs(b, K, NW, general, wpb, lds, s);
+        break;
+      case FSCHED_LJF:
+        e = pre ? fs::launch_sim_ljf_prefill(b, K, NW, general, wpb, lds, s)
+                : fs::launch_sim_ljf(b, K, NW, general, wpb, lds, s);
+        break;
       case FSCHED_ISJL:
-        e = upper ? fs::launch_sim_isjl_robust(b, K, NW, general, wpb, lds, s)
+        if (upper)
+          e = pre ? fs::launch_sim_isjl_robust_prefill(b, K, NW, general, wpb, lds, s)
+                  : fs::launch_sim_isjl_robust(b, K, NW, general, wpb, lds, s);
+        else
+          e = pre ? fs::launch_sim_isjl_prefill(b, K, NW, general, wpb, lds, s)
                   : fs::launch_sim_isjl(b, K, NW, general, wpb, lds, s);
         break;
-      default: e = fs::launch_sim_sjf(b, K, NW, general, wpb, lds, s); break;
+      default:
+        e = pre ? fs::launch_sim_sjf_prefill(b, K, NW, general, wpb, lds, s)
+                : fs::launch_sim_sjf(b, K, NW, general, wpb, lds, s);
+        break;
     }
     if (e != hipSuccess) return hip_fail(e);
   }
@@ -241,6 +256,7 @@ int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs
                           void* stream) {
   int rc = check_params(p, false);
   if (rc) return rc;
+  if (p->flags & FSCHED_F_PREFILL) return FSCHED_ENOTIMPL;  // chunked reading only
   if (n_inst < 0 || n_jobs < 1) return FSCHED_EINVAL;
   if (n_inst == 0) return FSCHED_OK;
   if (!arrival || !prompt || !output || !start || !out || !violation) return FSCHED_EINVAL;
@@ -301,6 +317,7 @@ int fsched_bruteforce_opt(const fsched_params* p, int64_t n_inst, int32_t n_jobs
                           int64_t* T_opt, int32_t* start_opt, void* stream) {
   int rc = check_params(p, false);
   if (rc) return rc;
+  if (p->flags & FSCHED_F_PREFILL) return FSCHED_ENOTIMPL;  // chunked reading only
   if (n_inst < 0 || n_jobs < 1) return FSCHED_EINVAL;
   if (n_jobs > fs::OPT_MAX_JOBS) return FSCHED_ETOOLARGE;
   if (n_inst == 0) return FSCHED_OK;

@@ -53,6 +53,17 @@ hipError_t launch_sim_isjl(const SimArgs& a, int K, int NW, bool general, int wa
 // Robust-ISJL (Section 3.4): ISJL planning on prompt + upper[i].
 hipError_t launch_sim_isjl_robust(const SimArgs& a, int K, int NW, bool general,
                                   int waves_per_block, size_t lds_bytes, hipStream_t s);
+// The prefill-at-admission variant of each policy (and of Robust-ISJL).
+hipError_t launch_sim_fcfs_prefill(const SimArgs& a, int K, int NW, bool general,
+                                   int waves_per_block, size_t lds_bytes, hipStream_t s);
+hipError_t launch_sim_ljf_prefill(const SimArgs& a, int K, int NW, bool general,
+                                  int waves_per_block, size_t lds_bytes, hipStream_t s);
+hipError_t launch_sim_isjl_prefill(const SimArgs& a, int K, int NW, bool general,
+                                   int waves_per_block, size_t lds_bytes, hipStream_t s);
+hipError_t launch_sim_sjf_prefill(const SimArgs& a, int K, int NW, bool general,
+                                  int waves_per_block, size_t lds_bytes, hipStream_t s);
+hipError_t launch_sim_isjl_robust_prefill(const SimArgs& a, int K, int NW, bool general,
+                                          int waves_per_block, size_t lds_bytes, hipStream_t s);
 hipError_t launch_sim_sjf(const SimArgs& a, int K, int NW, bool general, int waves_per_block,
                           size_t lds_bytes, hipStream_t s);
 

@@ -150,12 +150,20 @@ struct PoolBits {
 struct SimState {
   int t, ndone, nact, min_s, max_s, min_end;
   int64_t res, sum_s, sum_comp;
+  // prefill variant: largest prompt - start and summed prompt of the active jobs
+  // (the largest footprint at step t is t + G + 1)
+  int G;
+  int64_t sp;
 };
 
 // ROB: Robust-ISJL (Section 3.4): ordering, packs, caps and the KV reservation
 // use prompt + the predicted upper bound of the output; each job still runs its
 // true length, and fairness is checked on true progress.
-template <int POL, int K, int NW, bool GEN, bool ROB>
+// PRE: the prompt is prefilled at admission (Section 1 with eq. (1)'s decode
+// progress): a job runs one step per output token, reserves prompt + output and
+// its footprint in the batch cost is prompt + progress; fairness stays on
+// progress.  The sweeps are off (completions are taken one event at a time).
+template <int POL, int K, int NW, bool GEN, bool ROB, bool PRE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 : 1))) void simulate_kernel(SimArgs a) {
   static_assert(!ROB || POL == POL_ISJL, "predicted sizes: ISJL only");
   extern __shared__ uint32_t lds_raw[];
@@ -177,7 +185,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
   const int32_t* O = a.output + row;
   const int32_t* U = ROB ? a.upper + row : nullptr;  // predicted upper bounds of the outputs
   // true service length of job j (ROB: the length that plans used was larger)
-  auto true_len = [&](int j, int plan) -> int { return ROB ? P[j] + O[j] : plan; };
+  auto true_len = [&](int j, int plan) -> int {
+    return ROB ? (PRE ? O[j] : P[j] + O[j]) : plan;
+  };
+  // KV reservation of job j planned with size `plan`
+  auto resv_len = [&](int j, int plan) -> int { return PRE ? P[j] + plan : plan; };
 
   if (GEN) {  // only instances the sorted-arrival kernel deferred
     const int64_t prev = a.out_T ? a.out_T[inst] : a.out[inst].T;
@@ -190,7 +202,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
   // (arrival, index), or (len, index) in arrival order when arrivals are
   // sorted); padding keys sort last.
   const int NP = a.NP;
-  int bad = 0, big = 0, unsorted = 0, maxlen = 0, maxarr = 0;
+  int bad = 0, big = 0, unsorted = 0, maxlen = 0, maxfoot = 0, maxarr = 0;
   int64_t osum = 0, qsum = 0, rsum = 0;
   int carry_ar = 0;
   for (int i0 = 0; i0 < NP; i0 += WAVE) {
@@ -204,14 +216,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
     uint32_t key = 0xFFFFFFFFu;
     if (in) {
       bad |= (ar < 0) | (p < 0) | (o < 1) | (u < o);
-      const int64_t len = (int64_t)p + (int64_t)o;
-      const int64_t plan_len = (int64_t)p + (int64_t)u;
-      big |= (plan_len >= LEN_LIMIT);
+      // service length, planning size and largest footprint
+      const int64_t len = PRE ? (int64_t)o : (int64_t)p + (int64_t)o;
+      const int64_t plan_len = PRE ? (int64_t)u : (int64_t)p + (int64_t)u;
+      const int64_t foot = (int64_t)p + (int64_t)u;
+      big |= (foot >= LEN_LIMIT);
       unsorted |= (prev > ar);
-      if (len < LEN_LIMIT && len > maxlen) maxlen = (int)len;
+      if (foot < LEN_LIMIT && len > maxlen) maxlen = (int)len;
+      if (foot < LEN_LIMIT && foot > maxfoot) maxfoot = (int)foot;
       if (ar > maxarr) maxarr = ar;
-      osum += len;
-      qsum += len * (len + 1) / 2;
+      osum += (int64_t)p + (int64_t)o;  // tokens served
+      // Q: the footprint summed over the job's own steps (Theorem 5.1)
+      qsum += PRE ? (int64_t)o * p + (int64_t)o * (o + 1) / 2 : len * (len + 1) / 2;
       rsum += ar;
       const uint32_t l32 = (uint32_t)(ROB ? plan_len : len) & LMASK;
       if (POL == POL_LJF || POL == POL_ISJL) key = ((LMASK - l32) << 12) | (uint32_t)i;
@@ -237,6 +253,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
     return;
   }
   maxlen = wave_max(maxlen);
+  maxfoot = wave_max(maxfoot);
   maxarr = wave_max(maxarr);
   osum = wave_sum64(osum);
   qsum = wave_sum64(qsum);
@@ -254,8 +271,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       write_marker(a.out, a.out_T, inst, FSCHED_T_TOOLARGE, lane);
       return;
     }
-    double cb = (double)a.c * tb + (double)a.tau * (double)osum * (double)maxlen;
-    double wb = (double)a.c * tb + (double)a.tau * tb * (double)maxlen;
+    double cb = (double)a.c * tb + (double)a.tau * (double)osum * (double)maxfoot;
+    double wb = (double)a.c * tb + (double)a.tau * tb * (double)maxfoot;
     if (cb > 4.0e18 || wb > 4.0e18) {
       write_marker(a.out, a.out_T, inst, FSCHED_T_RANGE, lane);
       return;
@@ -281,7 +298,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       uint32_t len;
       if (POL == POL_LJF || POL == POL_ISJL) len = LMASK - (key >> 12);
       else if (POL == POL_SJF) len = key >> 12;
-      else len = (uint32_t)(P[id] + O[id]);
+      else len = (uint32_t)(PRE ? O[id] : P[id] + O[id]);
       W[r] = (len << 12) | (uint32_t)id;
       if (GEN) ARR[r] = A[id];
     }
@@ -293,12 +310,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
   const int alpha = a.alpha;
   const int64_t M = a.M;
   int ws_start[K], ws_end[K];
-  int ws_plan[K];  // ROB: planning size of the running job (its KV reservation)
+  int ws_plan[K];  // ROB: KV reservation of the running job (from its planning size)
+  int ws_p[K];     // PRE: prompt of the running job (its footprint offset)
   uint32_t ws_q[K];
   bool valid[K];
 #pragma unroll
   for (int k = 0; k < K; ++k) {
     ws_plan[k] = 0;
+    ws_p[k] = 0;
     ws_start[k] = IDLE;
     ws_end[k] = IDLE;
     ws_q[k] = QNONE | (QNONE << 16);
@@ -339,6 +358,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
   S.res = 0;
   S.sum_s = 0;
   S.sum_comp = 0;
+  S.G = -IDLE;
+  S.sp = 0;
   int64_t acc_E = 0, acc_C = 0, acc_W = 0, acc_ext = 0, acc_busy = 0, acc_peak = 0, acc_unfair = 0;
   int acc_maxext = 0, acc_maxact = 0;
   int32_t* st_out = a.start ? a.start + row : nullptr;
@@ -358,7 +379,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
     } else if (j < n) {
       // rank of job j: position of its priority key in W (binary search)
       rel_t = A[j];
-      uint32_t len = (uint32_t)(P[j] + (ROB ? U[j] : O[j]));
+      uint32_t len = (uint32_t)((PRE ? 0 : P[j]) + (ROB ? U[j] : O[j]));
       uint32_t key;
       if (POL == POL_SJF) key = (len << 12) | (uint32_t)j;
       else key = ((LMASK - len) << 12) | (uint32_t)j;
@@ -414,7 +435,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       int64_t run = S.res;
       for (int c0 = 0; c0 < G; c0 += WAVE) {
         const int j = c0 + lane;
-        const int len = j < G ? plen(W[STG[j]]) : 0;
+        int len = 0;
+        if (j < G) {
+          const uint32_t wv = W[STG[j]];
+          len = resv_len(pid(wv), plen(wv));
+        }
         const int pre = wave_scan_incl(len);
         const bool fail = j < G && (j > 0 || S.nact > 0) && (run + pre > M);
         const uint64_t fm = ballot(fail);
@@ -429,7 +454,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       tot64 = run - S.res;
     }
     if (na == 0) return 0;
-    int base = 0, lsum = 0, lplan = 0, lmin = IDLE;
+    int base = 0, lsum = 0, lplan = 0, lmin = IDLE, lp = 0, lpmax = -IDLE;
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       if (base < na) {
@@ -445,17 +470,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
           ws_end[k] = t + len;
           emit(pid(wv), t, len);
           lsum += len;
-          if (ROB) {
-            ws_plan[k] = plan;
-            lplan += plan;
+          if (ROB || PRE) {
+            const int rv = resv_len(pid(wv), plan);
+            ws_plan[k] = rv;
+            lplan += rv;
             lmin = min(lmin, len);
+          }
+          if (PRE) {
+            const int pp = P[pid(wv)];
+            ws_p[k] = pp;
+            lp += pp;
+            lpmax = max(lpmax, pp);
           }
         }
         base += __builtin_popcountll(bm);
       }
     }
-    int tot, ptot;  // true and planned lengths admitted
-    if (ROB) {
+    int tot, ptot;  // true lengths and reservations admitted
+    if (ROB || PRE) {
       tot = wave_sum(lsum);
       ptot = tot64 >= 0 ? (int)tot64 : wave_sum(lplan);
       adm_minlen = min(adm_minlen, wave_min(lmin));
@@ -464,6 +496,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       // the gathered jobs are in priority order, so the shortest admitted one
       // is the last (longest first) or the first (SJF)
       adm_minlen = min(adm_minlen, plen(W[STG[POL == POL_SJF ? 0 : na - 1]]));
+    }
+    if (PRE) {
+      S.sp += wave_sum(lp);
+      S.G = max(S.G, wave_max(lpmax) - t);  // na >= 1 jobs were admitted
     }
     pool.clear_upto(STG[na - 1], lane);  // the first na queued ranks
     qcount -= na;
@@ -480,15 +516,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
     if (S.min_end == t) {
       // the earliest / latest start is searched again only if a job holding
       // it retires
-      int nret = 0, lsum = 0, lplan = 0, me = IDLE;
-      bool hmin = false, hmax = false;
+      int nret = 0, lsum = 0, lplan = 0, lp = 0, me = IDLE;
+      bool hmin = false, hmax = false, hG = false;
 #pragma unroll
       for (int k = 0; k < K; ++k) {
         const bool r = ws_end[k] == t;
         nret += __builtin_popcountll(ballot(r));
         if (r) {
           lsum += ws_end[k] - ws_start[k];
-          if (ROB) lplan += ws_plan[k];
+          if (ROB || PRE) lplan += ws_plan[k];
+          if (PRE) {
+            lp += ws_p[k];
+            hG |= ws_p[k] - ws_start[k] == S.G;
+          }
           hmin |= ws_start[k] == S.min_s;
           hmax |= ws_start[k] == S.max_s;
           ws_end[k] = IDLE;
@@ -511,9 +551,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
           if (ws_start[k] != IDLE) mx = max(mx, ws_start[k]);
         S.max_s = wave_max(mx);
       }
+      if (PRE) {
+        S.sp -= wave_sum(lp);
+        if (ballot(hG)) {
+          int g = -IDLE;
+#pragma unroll
+          for (int k = 0; k < K; ++k)
+            if (ws_end[k] != IDLE) g = max(g, ws_p[k] - ws_start[k]);
+          S.G = wave_max(g);
+        }
+      }
       S.ndone += nret;
       S.nact -= nret;
-      S.res -= ROB ? wave_sum(lplan) : lret;
+      S.res -= (ROB || PRE) ? wave_sum(lplan) : lret;
       S.sum_s -= (int64_t)nret * t - (int64_t)lret;
     }
     if (S.ndone == n) break;
@@ -586,7 +636,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
         int r = head + done + lane;
         uint32_t wv = lane < c ? W[r] : 0u;
         int len = plen(wv), id = pid(wv);
-        int pre = wave_scan_incl(len);
+        const int pp = (PRE && lane < c) ? P[id] : 0;  // prompt (prefill variant)
+        int pre = wave_scan_incl(len + pp);            // reservations
         bool fit = (M == 0) || ((int64_t)(S.res + pre) <= M) ||
                    (S.nact == 0 && done == 0 && lane == 0);
         uint64_t fm = ballot(lane < c && !fit);
@@ -601,18 +652,30 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
               int idx = base + mbcnt(bm);
               int src = min(idx, WAVE - 1);
               int l2 = __shfl(len, src), id2 = __shfl(id, src);
+              const int p2 = PRE ? __shfl(pp, src) : 0;
               if (idle && idx < take) {
                 ws_start[k] = t;
                 ws_end[k] = t + l2;
+                if (PRE) {
+                  ws_p[k] = p2;
+                  ws_plan[k] = p2 + l2;
+                }
                 emit(id2, t, l2);
               }
               base += __builtin_popcountll(bm);
             }
           }
-          int tl = readlane(pre, take - 1);
+          int tl = readlane(pre, take - 1);  // reservations admitted
           adm_minlen = min(adm_minlen, wave_min(lane < take ? len : IDLE));
           adm += take;
-          adm_len += tl;
+          if (PRE) {
+            const int lp = wave_sum(lane < take ? pp : 0);
+            adm_len += tl - lp;
+            S.sp += lp;
+            S.G = max(S.G, wave_max(lane < take ? pp : -IDLE) - t);
+          } else {
+            adm_len += tl;
+          }
           S.res += tl;
           S.nact += take;
         }
@@ -656,7 +719,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
             for (int k = 0; k < K; ++k) {
               if (k * WAVE < G && Bp == G) {
                 const int j = k * WAVE + lane;
-                const int pre = wave_scan_incl(glen[k]);
+                // reservation of gathered job j (prefill variant: + prompt)
+                const int rv = (PRE && j < G) ? glen[k] + P[pid(W[STG[j]])] : glen[k];
+                const int pre = wave_scan_incl(rv);
                 const uint64_t fm = ballot(j < G && j >= 1 && run + pre > M);
                 if (fm) Bp = k * WAVE + __builtin_ctzll(fm);
                 else run += readlane(pre, 63);
@@ -821,7 +886,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
           int w = k * WAVE + lane;
           uint32_t h = ws_q[k] & 0xFFFFu;
           cand[k] = valid[k] && ws_end[k] == IDLE && h != QNONE && !(w == 0 && t < t_w1);
-          clen[k] = cand[k] ? plen(W[h]) : 0;
+          clen[k] = 0;  // reservation
+          if (cand[k]) {
+            const uint32_t wv = W[h];
+            clen[k] = resv_len(pid(wv), plen(wv));
+          }
           csum += clen[k];
           ccnt += cand[k] ? 1 : 0;
         }
@@ -853,7 +922,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
             tot = (int)(rres - S.res);
             ncand = nk;
           }
-          int mlen = IDLE, ltrue = 0;
+          int mlen = IDLE, ltrue = 0, lp = 0, lpmax = -IDLE;
 #pragma unroll
           for (int k = 0; k < K; ++k) {
             if (cand[k]) {
@@ -863,9 +932,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
               const int len = true_len(pid(wv), plan);
               ws_start[k] = t;
               ws_end[k] = t + len;
-              if (ROB) {
-                ws_plan[k] = plan;
+              if (ROB || PRE) {
+                ws_plan[k] = clen[k];
                 ltrue += len;
+              }
+              if (PRE) {
+                const int pp = P[pid(wv)];
+                ws_p[k] = pp;
+                lp += pp;
+                lpmax = max(lpmax, pp);
               }
               mlen = min(mlen, len);
               emit(pid(wv), t, len);
@@ -875,8 +950,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
           }
           adm_minlen = min(adm_minlen, wave_min(mlen));
           adm += ncand;
-          adm_len += ROB ? wave_sum(ltrue) : tot;
+          adm_len += (ROB || PRE) ? wave_sum(ltrue) : tot;
           S.res += tot;
+          if (PRE) {
+            // the KV check may have dropped every candidate
+            const int gm = wave_max(lpmax);
+            if (gm != -IDLE) S.G = max(S.G, gm - t);
+            S.sp += wave_sum(lp);
+          }
           S.nact += ncand;
           planned -= ncand;
         }
@@ -937,7 +1018,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
                           readlane(ws_end[0], 0) == IDLE &&
                           ((uint32_t)readlane((int)ws_q[0], 0) & 0xFFFFu) != QNONE;
     int quiet = 0;  // completions up to the next release, when nothing waits
-    if (POL != POL_LJF && S.nact > 0 &&
+    if (!PRE && POL != POL_LJF && S.nact > 0 &&
         (POL == POL_FCFS ? head == relk
                          : (qcount == 0 && (POL != POL_ISJL || (mode == 0 && planned == 0))))) {
       int r_next = IDLE;
@@ -955,7 +1036,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
           quiet += __builtin_popcountll(ballot(ws_end[k] != IDLE && ws_end[k] <= r_next));
       }
     }
-    bool sweep = (POL == POL_LJF || (POL == POL_ISJL && mode == 1 && !w0_timer) || quiet >= 3) &&
+    bool sweep = !PRE &&
+                 (POL == POL_LJF || (POL == POL_ISJL && mode == 1 && !w0_timer) || quiet >= 3) &&
                  S.nact > 0;
     if (sweep) {
       const int N = S.nact;
@@ -1212,9 +1294,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       acc_W += a.c * D;
     } else {
       const int64_t s = S.nact;
-      const int64_t m0 = (int64_t)(t - S.min_s) + 1;
+      // largest footprint at step t (it grows by one per step of the span) and
+      // the span's externality: each active job pays the largest footprint
+      // minus its own, a constant over the span
+      int64_t m0, xe;
+      if (PRE) {
+        m0 = (int64_t)t + S.G + 1;
+        xe = s * (int64_t)S.G - (S.sp - S.sum_s);
+      } else {
+        m0 = (int64_t)(t - S.min_s) + 1;
+        xe = S.sum_s - s * (int64_t)S.min_s;
+      }
       const int64_t sm = D * m0 + D * (D - 1) / 2;
-      acc_E += D * (S.sum_s - s * (int64_t)S.min_s);
+      acc_E += D * xe;
       acc_C += a.c * D + a.tau * s * sm;
       acc_W += a.c * D + a.tau * sm;
       const int ext = S.max_s - S.min_s;
@@ -1223,7 +1315,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       if (ext > alpha) acc_unfair += D;
       acc_maxext = max(acc_maxext, ext);
       acc_maxact = max(acc_maxact, S.nact);
-      acc_peak = max(acc_peak, s * (int64_t)tn - S.sum_s);
+      acc_peak = max(acc_peak, s * (int64_t)tn - S.sum_s + (PRE ? S.sp : 0));
     }
     S.t = tn;
   }
@@ -1254,14 +1346,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
   }
 }
 
-template <int POL, bool ROB = false>
+template <int POL, bool ROB = false, bool PRE = false>
 hipError_t launch_sim(const SimArgs& a, int K, int NW, bool general, int wpb, size_t lds,
                       hipStream_t s) {
   const int64_t blocks = (a.n_inst + wpb - 1) / wpb;
   dim3 grid((unsigned)blocks), block((unsigned)(wpb * WAVE));
 #define FS_LAUNCH(KK, NN, GG)                                                        \
   if (K == KK && NW == NN && general == GG) {                                        \
-    hipLaunchKernelGGL((simulate_kernel<POL, KK, NN, GG, ROB>), grid, block, lds, s, a);  \
+    hipLaunchKernelGGL((simulate_kernel<POL, KK, NN, GG, ROB, PRE>), grid, block, lds, s, a);  \
     return hipGetLastError();                                                        \
   }
 #define FS_LAUNCH_K(KK) \
