@@ -205,11 +205,36 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
   int bad = 0, big = 0, unsorted = 0, maxlen = 0, maxfoot = 0, maxarr = 0;
   int64_t osum = 0, qsum = 0, rsum = 0;
   int carry_ar = 0;
-  for (int i0 = 0; i0 < NP; i0 += WAVE) {
+  // The rows are software-pipelined: the loads of row r + PF are issued
+  // while row r is processed, so PF rows of loads are in flight (clamped
+  // indices keep every load in bounds; the rows past NP are never used).
+  constexpr int PF = 4;
+  int pf_a[PF], pf_p[PF], pf_o[PF], pf_u[PF];
+#pragma unroll
+  for (int d = 0; d < PF; ++d) {
+    const int ic = min(d * WAVE + lane, n - 1);
+    pf_a[d] = A[ic];
+    pf_p[d] = P[ic];
+    pf_o[d] = O[ic];
+    pf_u[d] = ROB ? U[ic] : 0;
+  }
+  for (int r0 = 0; r0 < NP; r0 += PF * WAVE) {
+#pragma unroll
+  for (int d = 0; d < PF; ++d) {
+    const int i0 = r0 + d * WAVE;
+    if (i0 >= NP) break;
     const int i = i0 + lane;
     const bool in = i < n;
-    const int ar = in ? A[i] : 0x7FFFFFFF, p = in ? P[i] : 0, o = in ? O[i] : 1;
-    const int u = (ROB && in) ? U[i] : o;
+    const int ar0 = pf_a[d], p0 = pf_p[d], o0 = pf_o[d], u0 = ROB ? pf_u[d] : o0;
+    {
+      const int ic = min(i + PF * WAVE, n - 1);
+      pf_a[d] = A[ic];
+      pf_p[d] = P[ic];
+      pf_o[d] = O[ic];
+      if (ROB) pf_u[d] = U[ic];
+    }
+    const int ar = in ? ar0 : 0x7FFFFFFF, p = in ? p0 : 0, o = in ? o0 : 1;
+    const int u = in ? u0 : o;
     int prev = __shfl_up(ar, 1);
     if (lane == 0) prev = i0 > 0 ? carry_ar : ar;
     carry_ar = readlane(ar, WAVE - 1);
@@ -236,6 +261,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       else key = (l32 << 12) | (uint32_t)i;
     }
     W[i] = key;
+  }
   }
   bad = ballot(bad != 0) != 0;
   big = ballot(big != 0) != 0;
