@@ -68,23 +68,58 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
   const int32_t* O = a.output + row;
   const int32_t* S0 = a.start + row;
 
+  // One pass over the job table: validation, instance totals, the two event
+  // keys of every job (end: (s + len, 0, i), start: (s, 1, i); they are only
+  // sorted once the table is known to be valid) and the lengths.  The rows are
+  // software-pipelined: the loads of row r + PF are issued while row r is
+  // processed (clamped indices keep every load in bounds).
+  const int NE = 2 * n, NP2 = a.NP2;
   int bad = 0, neg = 0, early = 0, big = 0, maxlen = 0;
   int64_t osum = 0, qsum = 0, csum = 0, lsum = 0, tmax = 0;
-  for (int i = lane; i < n; i += WAVE) {
-    int ar = A[i], p = P[i], o = O[i], s = S0[i];
-    bad |= (ar < 0) | (p < 0) | (o < 1);
-    int64_t len = (int64_t)p + (int64_t)o;
-    big |= (len >= (1 << 20));
-    neg |= (s < 0);
-    early |= (s < ar);
-    int64_t e = (int64_t)s + len;
-    if (e > tmax) tmax = e;
-    if (len < (1 << 20) && len > maxlen) maxlen = (int)len;
-    osum += len;
-    qsum += len * (len + 1) / 2;
-    csum += e;
-    lsum += e - ar;
+  constexpr int PF = 4;
+  int pf_a[PF], pf_p[PF], pf_o[PF], pf_s[PF];
+#pragma unroll
+  for (int d = 0; d < PF; ++d) {
+    const int ic = min(d * WAVE + lane, n - 1);
+    pf_a[d] = A[ic];
+    pf_p[d] = P[ic];
+    pf_o[d] = O[ic];
+    pf_s[d] = S0[ic];
   }
+  for (int r0 = 0; r0 < n; r0 += PF * WAVE) {
+#pragma unroll
+    for (int d = 0; d < PF; ++d) {
+      const int i0 = r0 + d * WAVE;
+      if (i0 >= n) break;
+      const int i = i0 + lane;
+      const int ar = pf_a[d], p = pf_p[d], o = pf_o[d], s = pf_s[d];
+      {
+        const int ic = min(i + PF * WAVE, n - 1);
+        pf_a[d] = A[ic];
+        pf_p[d] = P[ic];
+        pf_o[d] = O[ic];
+        pf_s[d] = S0[ic];
+      }
+      if (i < n) {
+        bad |= (ar < 0) | (p < 0) | (o < 1);
+        int64_t len = (int64_t)p + (int64_t)o;
+        big |= (len >= (1 << 20));
+        neg |= (s < 0);
+        early |= (s < ar);
+        int64_t e = (int64_t)s + len;
+        if (e > tmax) tmax = e;
+        if (len < (1 << 20) && len > maxlen) maxlen = (int)len;
+        osum += len;
+        qsum += len * (len + 1) / 2;
+        csum += e;
+        lsum += e - ar;
+        EV[2 * i] = ((uint32_t)(s + p + o) << 13) | (uint32_t)i;
+        EV[2 * i + 1] = ((uint32_t)s << 13) | (1u << 12) | (uint32_t)i;
+        LEN[i] = p + o;
+      }
+    }
+  }
+  for (int e = NE + lane; e < NP2; e += WAVE) EV[e] = 0xFFFFFFFFu;
   bad = ballot(bad != 0) != 0;
   neg = ballot(neg != 0) != 0;
   early = ballot(early != 0) != 0;
@@ -134,19 +169,7 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
     }
   }
 
-  // ---- events ---------------------------------------------------------------
-  const int NE = 2 * n, NP2 = a.NP2;
-  for (int e = lane; e < NP2; e += WAVE) {
-    uint32_t key = 0xFFFFFFFFu;
-    if (e < NE) {
-      int i = e >> 1;
-      int s = S0[i];
-      if (e & 1) key = ((uint32_t)s << 13) | (1u << 12) | (uint32_t)i;
-      else key = ((uint32_t)(s + P[i] + O[i]) << 13) | (uint32_t)i;
-    }
-    EV[e] = key;
-  }
-  for (int i = lane; i < n; i += WAVE) LEN[i] = P[i] + O[i];
+  // ---- events (keys written above) ---------------------------------------------
   wave_lds_sync();
   switch (NP2) {  // register sort up to 64 keys per lane, LDS network beyond
     case 64: wave_reg_sort<1>(EV, lane); break;
