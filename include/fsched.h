@@ -14,7 +14,8 @@
  *     Algorithm 3 for B >= 2), run on the released queue (Section 3.5,
  *     Online-ISJL), plus the unfair baselines FCFS and SJF of Section 2.1;
  *   - Section 5: the cost of step t is c + tau |S_t| max_{S_t} r_i with
- *     r_i = a_i + 1, and Theorem 5.1 splits the total into tau Q + c T + tau E.
+ *     r_i = a_i + 1, and the profit-decomposition theorem splits the total into
+ *     tau Q + c T + tau E.
  * In addition to the paper's model every call takes a KV budget M_kv: the
  * reservations (full lengths) of co-running requests must fit in M_kv unless a
  * request runs alone.

@@ -16,7 +16,8 @@
  *   - FCFS / SJF: the examples of Section 2.1 and the continuous-batching remark
  *     that follows them;
  *   - cost accounting: Section 5, eq. (batch cost c + tau |S| max r), the
- *     intrinsic term Q and the batching externality E of Theorem 5.1;
+ *     intrinsic term Q and the batching externality E of the profit-decomposition
+ *     theorem;
  *   - exact optimum: Appendix A (the integer program), extended with release
  *     steps and the KV budget.
  * Where the paper is silent or inconsistent the readings recorded in the design
@@ -124,7 +125,8 @@ static void finish_metrics(or_metrics* m, const or_inst* I, const or_acc* a, int
   for (int32_t i = 0; i < I->n; ++i) {
     int64_t l = I->len[i], q = I->pre ? I->pre[i] : 0;
     O += q + l; /* tokens served */
-    /* Q = sum_i of the footprint summed over the job's own steps, Theorem 5.1:
+    /* Q = sum_i of the footprint summed over the job's own steps (profit
+     * decomposition, Section 5):
      * sum_{k=1..l_i} (q_i + k) */
     Q += l * q + l * (l + 1) / 2;
     sc += start[i] + l;

@@ -1,4 +1,4 @@
-// Re-scoring of given schedules (Section 5, Theorem 5.1; eq. (1) checks):
+// Re-scoring of given schedules (Section 5, profit decomposition; eq. (1) checks):
 // one wavefront per instance.
 //
 // The 2n start/end events are sorted (in registers, or in LDS beyond 4,096

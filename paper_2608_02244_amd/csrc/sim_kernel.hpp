@@ -251,7 +251,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       if (foot < LEN_LIMIT && foot > maxfoot) maxfoot = (int)foot;
       if (ar > maxarr) maxarr = ar;
       osum += (int64_t)p + (int64_t)o;  // tokens served
-      // Q: the footprint summed over the job's own steps (Theorem 5.1)
+      // Q: the footprint summed over the job's own steps (Section 5)
       qsum += PRE ? (int64_t)o * p + (int64_t)o * (o + 1) / 2 : len * (len + 1) / 2;
       rsum += ar;
       const uint32_t l32 = (uint32_t)(ROB ? plan_len : len) & LMASK;

@@ -4,7 +4,7 @@ Host post-processing of the exact integer metrics of ``fsched_simulate`` (the
 derived real-valued quantities are fp64 on the host):
 
 * revenue under linear token pricing: ``R = p0 * O`` (O = total tokens served);
-* cost by the decomposition of Section 5 (Theorem 5.1):
+* cost by the decomposition of Section 5 (the profit-decomposition theorem):
   ``C = tau * Q + c * T + tau * E``, Q the intrinsic (schedule-free) term, T the
   makespan, E the batching externality;
 * profit ``R - C``; throughput ``O / T``; average within-batch extent

@@ -169,7 +169,7 @@ def test_single_batch_closed_forms():
 
 
 def q_by_definition(lengths):
-    """Q = sum_i sum_{k=1}^{o_i} k (Theorem 5.1), by explicit summation."""
+    """Q = sum_i sum_{k=1}^{o_i} k (the profit-decomposition theorem, Section 5), by explicit summation."""
     return sum(sum(range(1, int(l) + 1)) for l in lengths)
 
 
@@ -179,7 +179,7 @@ POLICY_ALPHAS = [("fcfs", ALPHA_INF), ("sjf", ALPHA_INF), ("ljf", 0), ("ljf", 3)
 
 @pytest.mark.parametrize("policy,alpha", POLICY_ALPHAS)
 def test_decomposition_identity_and_invariants(policy, alpha):
-    """Theorem 5.1: C = cT + tau Q + tau E exactly; each job runs its length once so
+    """Profit-decomposition theorem (Section 5): C = cT + tau Q + tau E exactly; each job runs its length once so
     sum_t |S_t| = O; fair policies keep every step within alpha and E <= alpha O;
     capacity and the KV budget hold at every step."""
     rng = np.random.default_rng(zlib.crc32(f"{policy}:{alpha}".encode()))
@@ -216,7 +216,7 @@ def test_decomposition_identity_and_invariants(policy, alpha):
 
 
 def test_ljf_closed_form_and_ratio():
-    """Theorem 3.1 proof: offline, no KV budget, LJF's makespan is
+    """Proof of the LJF theorem (Section 3.1): offline, no KV budget, LJF's makespan is
     o_1 + o_{B+1} + o_{2B+1} + ... over the sorted lengths, E_LJF = 0 (Prop. on
     pairwise profit), and T_OPT / T_LJF >= B / (2B - 1)."""
     rng = np.random.default_rng(7)
@@ -307,7 +307,7 @@ def test_alpha_zero_is_ljf_and_optimal():
 def test_large_alpha_is_lpt_and_graham():
     """alpha >= max length: the fairness guard never binds, ISJL's Phase TWO is LPT
     list scheduling, its makespan is within (4/3 - 1/(3B)) of P||Cmax, which is
-    also the fair optimum (Proposition after Theorem 3.2, citing Graham 1969)."""
+    also the fair optimum (the proposition quoting Graham 1969, Section 3.2)."""
     rng = np.random.default_rng(12)
     for trial in range(60):
         n = int(rng.integers(1, 8))
@@ -398,7 +398,7 @@ def floor_beta_star(alpha):
 
 def test_b2_competitive_ratio_bounds():
     """B = 2 (Algorithm 2): with beta = alpha the ratio T_OPT/T_ISJL is at least 3/4
-    (Remark after Theorem 3.2); with the beta* flag it is at least Theorem 3.2's
+    (the remark on beta = alpha, Section 3.2); with the beta* flag it is at least the B = 2 theorem's
     bound at the integer beta used; LJF is at least B/(2B-1) = 2/3."""
     rng = np.random.default_rng(15)
     worst = Fraction(1)
@@ -425,11 +425,11 @@ def test_beta_star_floor_values():
 def test_recorded_findings():
     """Counterexamples found by this oracle to two of the paper's claims, each
     traced by hand (tests/golden/cr_findings.json has the traces):
-    - Theorem 3.3's curve CR(gamma) is not a lower bound at B = 2, beta = alpha;
+    - the gamma-curve CR(gamma) (Section 4) is not a lower bound at B = 2, beta = alpha;
     - with B = 3, where Algorithm 3's plan is fair only pairwise with o_1 and every
-      plan start is guarded, T_OPT/T_ISJL falls to 1/2 < 3/4 (Theorem 3.3's and
-      Theorem 3.4's claims for B >= 2);
-    - at B = 2 with beta = alpha the ratio falls to 26/35 < 3/4 (Theorem 3.1's
+      plan start is guarded, T_OPT/T_ISJL falls to 1/2 < 3/4 (the claim of the
+      general-B theorem, Section 3.3);
+    - at B = 2 with beta = alpha the ratio falls to 26/35 < 3/4 (the B = 2 theorem's
       bound at beta = alpha)."""
     with open(os.path.join(GOLDEN, "cr_findings.json")) as fh:
         cases = json.load(fh)

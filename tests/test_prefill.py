@@ -4,8 +4,8 @@ footprint is prompt + decode progress (the Section 5 batch cost takes the
 largest footprint), fairness (eq. (1)) is over decode progress, and a job
 reserves prompt + output of the KV budget.
 
-Pins: hand-traced examples, the chunked reading at zero prompts, Theorem 5.1's
-identity C = c T + tau (Q + E) with Q computed from the lengths alone, the
+Pins: hand-traced examples, the chunked reading at zero prompts, the profit-decomposition
+identity (Section 5) C = c T + tau (Q + E) with Q computed from the lengths alone, the
 single-worker case (no externality), fairness, and the schedule's validity
 against the budget and capacity."""
 import json

@@ -68,7 +68,7 @@ def table():
 
 
 def test_intrinsic_term_and_revenue_are_schedule_free(table):
-    """Theorem 5.1: Q does not depend on the schedule (nor does the revenue)."""
+    """Profit-decomposition theorem (Section 5): Q does not depend on the schedule (nor does the revenue)."""
     for r in range(3):
         rows = [table["metrics"][k][r] for k in table["metrics"]]
         assert len({int(x["Q"]) for x in rows}) == 1
