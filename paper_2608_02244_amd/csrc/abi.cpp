@@ -272,12 +272,23 @@ int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs
   a.c = p->cost_c;
   a.tau = p->cost_tau;
   a.NP2 = next_pow2(2 * n_jobs);
-  a.wave_words = a.NP2 + n_jobs;  // sorted events, then the length of each job
-  a.wave_words = (a.wave_words + 3) & ~3;
-  const size_t per_wave = (size_t)a.wave_words * 4;
-  int wpb = 4;
-  while (wpb > 1 && per_wave * wpb > 64 * 1024) wpb >>= 1;
-  const size_t lds = per_wave * wpb;
+  // Two passes: 16-bit job lengths in LDS, then 32-bit ones for the instances
+  // the first pass deferred (a job of 65,536 tokens or more).
+  auto launch = [&](const fs::DecArgs& d, hipStream_t st) -> hipError_t {
+    for (int narrow = 1; narrow >= 0; --narrow) {
+      fs::DecArgs b = d;
+      b.deferred_only = narrow ? 0 : 1;
+      // sorted events, then the length of each job
+      b.wave_words = b.NP2 + (narrow ? (n_jobs + 1) / 2 : n_jobs);
+      b.wave_words = (b.wave_words + 3) & ~3;
+      const size_t per_wave = (size_t)b.wave_words * 4;
+      int wpb = 4;
+      while (wpb > 1 && per_wave * wpb > 64 * 1024) wpb >>= 1;
+      hipError_t e = fs::launch_decompose(b, narrow != 0, wpb, per_wave * wpb, st);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  };
   if (p->flags & FSCHED_F_DEVICE_PTRS) {
     a.arrival = arrival;
     a.prompt = prompt;
@@ -285,7 +296,7 @@ int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs
     a.start = start;
     a.out = out;
     a.viol = violation;
-    hipError_t e = fs::launch_decompose(a, wpb, lds, s);
+    hipError_t e = launch(a, s);
     if (e != hipSuccess) return hip_fail(e);
     if (p->flags & FSCHED_F_SYNC) {
       e = hipStreamSynchronize(s);
@@ -302,7 +313,7 @@ int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs
   a.out = (fsched_metrics*)st.alloc((size_t)n_inst * sizeof(fsched_metrics));
   a.viol = (uint32_t*)st.alloc((size_t)n_inst * sizeof(uint32_t));
   if (st.err != hipSuccess) return hip_fail(st.err);
-  hipError_t e = fs::launch_decompose(a, wpb, lds, s);
+  hipError_t e = launch(a, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   if (e == hipSuccess)
     e = hipMemcpy(out, a.out, (size_t)n_inst * sizeof(fsched_metrics), hipMemcpyDeviceToHost);

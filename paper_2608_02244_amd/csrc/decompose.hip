@@ -9,6 +9,8 @@
 // two event times the active set is fixed and the Section 5 terms are summed
 // in closed form, as in the simulation kernel; the sweep itself is described
 // where it runs.
+#include <type_traits>
+
 #include "dec_common.hpp"
 #include "regsort.hpp"
 #include "wave.hpp"
@@ -53,6 +55,9 @@ __device__ inline void dec_marker(fsched_metrics* out, uint32_t* viol, int64_t i
 
 }  // namespace
 
+// NARROW: lengths are kept as 16-bit values (an instance with a job of 65,536
+// tokens or more is left to the wide pass).
+template <bool NARROW>
 __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
   extern __shared__ uint32_t lds_raw[];
   const int wib = threadIdx.x >> 6;
@@ -61,7 +66,9 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
   const int lane = lane_id();
   const int n = a.n;
   uint32_t* EV = lds_raw + (size_t)wib * (size_t)a.wave_words;
-  int32_t* LEN = (int32_t*)(EV + a.NP2);  // per job: prompt + output
+  using len_t = typename std::conditional<NARROW, uint16_t, int32_t>::type;
+  len_t* LEN = (len_t*)(EV + a.NP2);  // per job: prompt + output
+  if (!NARROW && a.deferred_only && a.out[inst].T != DEC_DEFERRED) return;
   const int64_t row = inst * (int64_t)n;
   const int32_t* A = a.arrival + row;
   const int32_t* P = a.prompt + row;
@@ -115,7 +122,7 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
         lsum += e - ar;
         EV[2 * i] = ((uint32_t)(s + p + o) << 13) | (uint32_t)i;
         EV[2 * i + 1] = ((uint32_t)s << 13) | (1u << 12) | (uint32_t)i;
-        LEN[i] = p + o;
+        LEN[i] = (len_t)(p + o);
       }
     }
   }
@@ -152,6 +159,10 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
     tmax = ((int64_t)hi << 31) | lo;
   }
   maxlen = wave_max(maxlen);
+  if (NARROW && maxlen >= 65536) {
+    dec_marker(a.out, a.viol, inst, DEC_DEFERRED, 0u, lane);
+    return;
+  }
   osum = wave_sum64(osum);
   qsum = wave_sum64(qsum);
   csum = wave_sum64(csum);
@@ -482,10 +493,14 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
   }
 }
 
-hipError_t launch_decompose(const DecArgs& a, int wpb, size_t lds, hipStream_t s) {
+hipError_t launch_decompose(const DecArgs& a, bool narrow, int wpb, size_t lds, hipStream_t s) {
   const int64_t blocks = (a.n_inst + wpb - 1) / wpb;
-  hipLaunchKernelGGL(decompose_kernel, dim3((unsigned)blocks), dim3((unsigned)(wpb * WAVE)), lds,
-                     s, a);
+  if (narrow)
+    hipLaunchKernelGGL(decompose_kernel<true>, dim3((unsigned)blocks), dim3((unsigned)(wpb * WAVE)),
+                       lds, s, a);
+  else
+    hipLaunchKernelGGL(decompose_kernel<false>, dim3((unsigned)blocks),
+                       dim3((unsigned)(wpb * WAVE)), lds, s, a);
   return hipGetLastError();
 }
 

@@ -150,3 +150,26 @@ def test_named_workload_schedules(dev, name):
     stn = st.cpu().numpy()[idx]
     ref, rv = oracle.decompose(a[idx], p[idx], o[idx], stn, **kw)
     same(name, dm[idx], ref, dv[idx].astype(np.uint32), rv)
+
+
+def test_long_jobs_take_the_wide_pass(dev):
+    """Jobs of 65,536 tokens or more do not fit the 16-bit lengths of the first
+    pass: their instances are scored by the second (32-bit) pass, next to rows
+    the first pass finishes; 65,535 and 65,536 sit on either side of the cut."""
+    rng = np.random.default_rng(77)
+    n = 40
+    a = np.zeros((6, n), np.int32)
+    p = rng.integers(0, 50, size=(6, n)).astype(np.int32)
+    o = rng.integers(1, 3000, size=(6, n)).astype(np.int32)
+    o[1, 7] = 65535 - p[1, 7]          # longest job exactly 65,535: first pass
+    o[2, 3] = 65536 - p[2, 3]          # exactly 65,536: second pass
+    o[3, ::5] = rng.integers(70000, 200000, size=o[3, ::5].shape)
+    o[5, 0] = 300000
+    s = (a + rng.integers(0, 40000, size=a.shape)).astype(np.int32)
+    for kw in (dict(B=4, alpha=ALPHA_INF), dict(B=0, alpha=1000, M_kv=500000, cost_c=3,
+                                                cost_tau=1)):
+        ref, rv = oracle.decompose(a, p, o, s, **kw)
+        got, gv = gpu_dec(dev, a, p, o, s, **kw)
+        same(f"long jobs {kw}", got, ref, gv, rv)
+        hm, hv = fs.cost_decompose(a, p, o, s, **kw)
+        same(f"long jobs host mode {kw}", hm, ref, hv, rv)
