@@ -397,9 +397,13 @@ def floor_beta_star(alpha):
 
 
 def test_b2_competitive_ratio_bounds():
-    """B = 2 (Algorithm 2): with beta = alpha the ratio T_OPT/T_ISJL is at least 3/4
-    (the remark on beta = alpha, Section 3.2); with the beta* flag it is at least the B = 2 theorem's
-    bound at the integer beta used; LJF is at least B/(2B-1) = 2/3."""
+    """B = 2 on 400 random instances of at most 6 jobs: LJF's ratio T_OPT/T is at
+    least B/(2B-1) = 2/3 (the LJF theorem, Section 3.1).  ISJL's ratio stays at or
+    above 3/4 with beta = alpha (the remark on beta = alpha, Section 3.2) and at or
+    above the B = 2 theorem's bound at the integer beta* used; those two are the
+    paper's claims, which fail on some 8-job instances (recorded in
+    tests/golden/cr_findings.json) but hold on this sample of smaller ones, so a
+    regression in the oracle's ISJL shows up here."""
     rng = np.random.default_rng(15)
     worst = Fraction(1)
     for trial in range(400):
