@@ -462,11 +462,27 @@ def time_decompose(torch, np, workload, fs, args) -> int:
         NP2 *= 2
     L = NP2.bit_length() - 1
     ops = float(w.n_inst) * (2 * (NP2 // 2) * L * (L + 1) // 2 + 4 * 2 * w.n_jobs)
-    print(json.dumps({"mode": "decompose", "workload": w.name, "ms_per_call": dt * 1e3,
-                      "instance_steps_per_s": steps_per_call / dt,
-                      "roofline": {"bound": "alu", "achieved": ops / dt / 1e12,
-                                   "peak": PEAK_ALU / 1e12, "frac": ops / dt / PEAK_ALU,
-                                   "ops_per_launch": ops}}))
+    out = {"mode": "decompose", "workload": w.name, "ms_per_call": dt * 1e3,
+           "instance_steps_per_s": steps_per_call / dt,
+           "roofline": {"bound": "alu", "achieved": ops / dt / 1e12, "peak": PEAK_ALU / 1e12,
+                        "frac": ops / dt / PEAK_ALU, "ops_per_launch": ops}}
+    if not args.no_cpu_baseline:
+        # the oracle's re-scorer on a bounded sample of the same schedules
+        import oracle
+        s_host = st.cpu().numpy()
+        T = fs.metrics_view(raw)["T"]
+        c0 = time.perf_counter()
+        oracle.decompose(a[:1], p[:1], o[:1], s_host[:1], **kw)
+        one = max(time.perf_counter() - c0, 1e-4)
+        k = int(max(1, min(w.n_inst, args.cpu_seconds / 3 / one)))
+        c0 = time.perf_counter()
+        ref, _ = oracle.decompose(a[:k], p[:k], o[:k], s_host[:k], **kw)
+        cpu_s = time.perf_counter() - c0
+        out["cpu_baseline"] = {"value": float(T[:k].sum()) / cpu_s, "unit": "instance-steps/s",
+                               "cores": 1, "kind": "oracle",
+                               "sample": f"first {k} of {w.n_inst} schedules, {cpu_s:.1f} s",
+                               "parity_on_sample": bool((ref["T"] == T[:k]).all())}
+    print(json.dumps(out))
     return 0
 
 
@@ -486,7 +502,25 @@ def time_opt(torch, np, workload, fs, args) -> int:
             torch.cuda.synchronize()
             dt = (time.perf_counter() - t0) / max(1, args.steps)
             res[f"M_kv={M},alpha={al}"] = {"s_per_call": dt, "solves_per_s": w.n_inst / dt}
-    print(json.dumps({"mode": "opt", "workload": w.name, "results": res}))
+    out = {"mode": "opt", "workload": w.name, "results": res}
+    if not args.no_cpu_baseline:
+        # the oracle's exhaustive optimum on a bounded sample (first setting)
+        import oracle
+        al, M = w.alphas[0], w.M_kv
+        c0 = time.perf_counter()
+        oracle.opt(a[:64], p[:64], o[:64], B=w.B, alpha=al, M_kv=M)
+        one = max((time.perf_counter() - c0) / 64, 1e-6)
+        k = int(max(64, min(w.n_inst, args.cpu_seconds / 3 / one)))
+        c0 = time.perf_counter()
+        ref = oracle.opt(a[:k], p[:k], o[:k], B=w.B, alpha=al, M_kv=M)
+        cpu_s = time.perf_counter() - c0
+        T_gpu, _ = fs.bruteforce_opt(ta[:k], tp[:k], to[:k], B=w.B, alpha=al, M_kv=M)
+        out["cpu_baseline"] = {"value": k / cpu_s, "unit": "exact solves/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": f"first {k} instances, M_kv={M}, alpha={al}, "
+                                         f"{cpu_s:.1f} s",
+                               "parity_on_sample": bool((T_gpu.cpu().numpy() == ref).all())}
+    print(json.dumps(out))
     return 0
 
 
