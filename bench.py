@@ -1,7 +1,7 @@
 """Benchmark: ISJL instance-steps per second on one MI355X.
 
-One step = one fsched_simulate call over the whole batch of the headline
-workload (65,536 instances x 2,000 jobs, heavy-tailed outputs, Poisson
+One step = one fsched_simulate call over the whole batch of the
+pareto_65536x2000 workload (65,536 instances x 2,000 jobs, heavy-tailed outputs, Poisson
 arrivals, B = 512, M_kv = 1,048,576, alpha = 128, affine integer step cost):
 ordering, event loop, admissions, Section 5 accounting and the per-instance
 metrics, with the job tables already resident in HBM.  An instance-step is one
@@ -90,10 +90,10 @@ def main() -> int:
                          "two library calls (for profiles); host: host-buffer calls, "
                          "PCIe copies included; profit: the linear-pricing experiment; "
                          "gamma: the competitive-ratio experiment; robust: Robust-ISJL on "
-                         "predicted sizes (headline workload and the guarantee on tiny "
+                         "predicted sizes (pareto_65536x2000 and the guarantee on tiny "
                          "instances); efficiency: throughput and AEL of every policy on the "
                          "LMSYS-shaped workload; prefill: the prefill-at-admission variant "
-                         "of every policy on the headline workload")
+                         "of every policy on pareto_65536x2000")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the instances are "
@@ -303,7 +303,7 @@ def time_gamma(args) -> int:
 
 
 def time_robust(torch, np, workload, fs, args) -> int:
-    """Robust-ISJL: (1) the headline workload with upper bounds u = o + U * slack * o
+    """Robust-ISJL: (1) the benchmark workload with upper bounds u = o + U * slack * o
     at several slacks, timed like the benchmark line, against ISJL on the true
     sizes (makespan and cost ratios, fairness); (2) the guarantee
     T_R <= 4/3 (T_OPT + Delta_pack), its corollary and the proof's first step on
@@ -333,7 +333,7 @@ def time_robust(torch, np, workload, fs, args) -> int:
         e1.record(stream)
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / args.steps
-        print(f"robust headline slack={slack}: {ms:.2f} ms", file=sys.stderr, flush=True)
+        print(f"robust {w.name} slack={slack}: {ms:.2f} ms", file=sys.stderr, flush=True)
         rows.append({"slack": slack, "ms_per_launch": ms,
                      "instance_steps_per_s": float(m["T"].sum()) / (ms / 1e3),
                      "T_over_isjl": float(m["T"].sum() / base["T"].sum()),
@@ -343,7 +343,7 @@ def time_robust(torch, np, workload, fs, args) -> int:
                      "unfair_steps": int(m["unfair_steps"].sum()),
                      "max_extent": int(m["max_extent"].max())})
         del tu
-    out = {"mode": "robust", "workload": w.name, "alpha": alpha, "headline": rows}
+    out = {"mode": "robust", "workload": w.name, "alpha": alpha, "full_size": rows}
     # the exhaustive optimum gets much slower with B, so fewer instances there
     tiny = []
     for B, n in ((2, 32768), (3, 4096), (4, 1024)):
@@ -383,7 +383,7 @@ def time_efficiency(np, workload) -> int:
 
 
 def time_prefill(torch, np, workload, fs, args) -> int:
-    """Every policy in the prefill-at-admission variant on the headline workload
+    """Every policy in the prefill-at-admission variant on the benchmark workload
     (the prompt is processed at admission, a job runs its output tokens), timed
     with HIP events, beside ISJL in the chunked reading."""
     w = workload.WORKLOADS[args.workload]
@@ -438,7 +438,7 @@ def copy_calibration(torch, steps: int) -> int:
 
 
 def time_decompose(torch, np, workload, fs, args) -> int:
-    """Re-score the ISJL schedules of the headline workload (fsched_cost_decompose)."""
+    """Re-score the ISJL schedules of the benchmark workload (fsched_cost_decompose)."""
     w = workload.WORKLOADS[args.workload]
     a, p, o = workload.generate(w)
     ta, tp, to = (torch.from_numpy(x).to("cuda:0") for x in (a, p, o))

@@ -2,7 +2,7 @@
 oracle, through the C ABI: every metric, start and finish step, bit-exact.
 Small random instances (offline, sorted and unsorted releases, KV budgets,
 alpha = 0 / infinity, the two job-bitmap widths and up to 16 worker slots per
-lane), exact predictions against fsched_simulate, the full-size headline
+lane), exact predictions against fsched_simulate, the full-size pareto_65536x2000
 workload with loose predictions (sampled instances against the oracle,
 fairness on all), error paths, and the experiment driver against the oracle's.
 """
@@ -91,7 +91,7 @@ def test_exact_predictions_equal_isjl(dev):
         assert_same(f"u = o alpha={alpha}", r, i, rs, is_, rf, if_)
 
 
-def test_headline_workload_with_loose_predictions(dev):
+def test_pareto_workload_with_loose_predictions(dev):
     import torch
     w = workload.WORKLOADS["pareto_65536x2000"]
     log("generate pareto_65536x2000")

@@ -109,7 +109,7 @@ WORKLOADS: Dict[str, Workload] = {w.name: w for w in [
     Workload("pareto_65536x2000", 4, 65536, 2000, 8.0,
              lognormal(1024.0, 0.8, 1, 16384), pareto(1.5, 8.0, 8192),
              B=512, M_kv=1048576, alphas=(128,), cost_c=1000, cost_tau=1,
-             policies=("isjl",), note="throughput headline"),
+             policies=("isjl",), note="throughput benchmark"),
     Workload("tiny_opt_1048576x8", 5, 1048576, 8, 0.0,
              uniform(1, 4), two_uniform(0.5, 1, 1, 1, 16),
              B=2, M_kv=16, alphas=(1, 2, 4), cost_c=0, cost_tau=1,
