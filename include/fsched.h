@@ -69,7 +69,7 @@ enum {
   FSCHED_EDEVICE = -4,   /* a HIP call failed (see fsched_last_hip_error)     */
   FSCHED_ETOOLARGE = -5, /* beyond a kernel limit                            */
   FSCHED_ENOTIMPL = -6,
-  FSCHED_EINTERNAL = -7  /* the event loop of an instance found no next event */
+  FSCHED_EINTERNAL = -7  /* an instance found no next event, or its exact search hit its cap */
 };
 
 /* Per-instance markers written into fsched_metrics.T in device mode. */
@@ -215,7 +215,10 @@ int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs
  * reservations within M_kv unless a job runs alone, and |s_i - s_j| <= alpha for
  * every pair active at a common step.  Exhaustive search over schedules in start
  * order with a memo and lower bounds, started from the ISJL schedule of the
- * instance (which is returned when nothing beats it).
+ * instance (which is returned when nothing beats it).  The search of one
+ * instance is capped at 2^22 steps; an instance that reaches the cap gets
+ * T_opt = FSCHED_T_INTERNAL (host mode: EINTERNAL).  No instance of the tiny
+ * workloads at B <= 3 comes near it; at B = 4 a few do.
  *   n_jobs     <= 8 (ETOOLARGE otherwise); every length <= 255 and every
  *              arrival <= 4095 (else T = FSCHED_T_TOOLARGE / ETOOLARGE).
  *   T_opt      [n_inst] int64 optimum makespan.

@@ -363,7 +363,7 @@ struct Dfs {
           set(depth + 1, F_FLAGS, 0u);
           wave_lds_sync();
           depth++;
-          if (++guard > GUARD) return -1;  // far above any search seen for n <= 8
+          if (++guard > GUARD) return -1;  // the cap: some 8-job searches at B = 4 reach it
           continue;
         }
         memo.put(ka, plo, phi, S, (uint32_t)best | ((best < bound) ? 0x80000000u : 0u), lane);
