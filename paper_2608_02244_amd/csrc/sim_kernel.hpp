@@ -428,6 +428,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
     if (fi_out) fi_out[id] = t + len;
   };
 
+  // Whether the first queued job (in priority order) cannot join the running
+  // ones under the KV budget: then a strict-prefix admission admits nothing,
+  // and the gather is skipped.  Checked with up to 4 slots per lane (B <= 256),
+  // where a blocked head is common and the gather is a large share of an event;
+  // the 8- and 16-slot kernels (at their register limit) gather regardless.
+  auto head_blocked = [&]() -> bool {
+    if (K > 4 || M == 0 || S.nact == 0) return false;
+    const int r = pool.first();
+    if (r < 0) return false;
+    const uint32_t wv = W[r];
+    return S.res + resv_len(pid(wv), plen(wv)) > M;
+  };
+
   // The first G queued ranks, in priority order, into STG[0..G).
   auto gather_first = [&](int G) {
     int gbase = 0;
@@ -715,7 +728,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
         if (freew > 0) {
           const int kp = qcount;
           const int G = min(freew, kp);
-          if (G > 0) {
+          if (G > 0 && !head_blocked()) {
             gather_first(G);
             admit_prefix(t, G, false, adm, adm_len, adm_minlen);
           }
@@ -1008,6 +1021,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
           if (kp > 0) {
             if (amax > alpha) {
               mode = 1;
+            } else if (head_blocked()) {
+              kv_block = true;
             } else {
               const int G = min(nie, kp);
               gather_first(G);
