@@ -19,7 +19,9 @@
 //   sum_S r     = |S| (t+1) - sum_s                            (largest at t+D-1)
 // Decisions are taken only at events; the step-by-step definition gives the
 // same decisions at the steps in between because nothing they depend on
-// changes there.
+// changes there.  (With the prompt prefilled at admission the largest
+// footprint is t + max(prompt_j - start_j) + 1 and E per step is
+// |S| G - sum_S (prompt_j - start_j), both constant between events.)
 //
 // Per-wave state:
 //   LDS   W[r]     jobs in the policy's priority order, packed (len << 12 | id)
@@ -27,7 +29,8 @@
 //         QN[r]    next job in the same ISJL plan queue (uint16, ISJL)
 //         STG[j]   gather buffer of the first queued ranks (uint16, not FCFS)
 //         PEND[i]  released ranks on their way into the bitmap (aliases STG)
-//   The drain sweep sorts the active slots in registers and needs no LDS.
+//   The drain sweep sorts the active slots in registers; up to 64 of them are
+//   first packed into one register through the gather buffer.
 //   VGPR  K worker slots per lane: worker w lives in slot w/64 of lane w%64
 //         (start, end, ISJL plan-queue head|tail); a bitmap of queued jobs over
 //         ranks (bit r%32 of word r/2048 in lane (r/32)%64).
