@@ -104,7 +104,10 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
   const int q_words = (isjl && p->alpha != FSCHED_ALPHA_INF) ? NP / 2 : 0;
   // gather buffer (uint16 per worker), also the release scatter buffer (one
   // word per 32 ranks)
-  const int stage_words = p->policy != FSCHED_FCFS ? std::max((Beff + 1) / 2, 64 * NW) : 0;
+  // FCFS gathers nothing, but with 4 or more slots per lane its sweeps pack up to
+  // 64 active slots through this buffer too
+  const int stage_words =
+      p->policy != FSCHED_FCFS ? std::max((Beff + 1) / 2, 64 * NW) : (K >= 4 ? 64 : 0);
 
   fs::SimArgs a;
   std::memset(&a, 0, sizeof(a));

@@ -552,6 +552,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
     return na;
   };
 
+  // Gather and admit the strict prefix of the first G queued jobs.  With up to 4
+  // slots per lane and a binding KV budget, the first 8 are gathered and scanned
+  // alone and the rest only if all 8 fit: admitting those 8 and then the prefix
+  // of the next G - 8 is the same strict prefix, and a budget that stops early
+  // spares the gather of all G.
+  auto admit_first = [&](int t, int G, bool need_empty_queue, int& adm, int64_t& adm_len,
+                         int& adm_minlen) -> int {
+    constexpr int G0 = 8;
+    if (K <= 4 && M != 0 && S.nact > 0 && G > G0) {
+      gather_first(G0);
+      const int na = admit_prefix(t, G0, need_empty_queue, adm, adm_len, adm_minlen);
+      if (na < G0) return na;
+      gather_first(G - G0);
+      return G0 + admit_prefix(t, G - G0, need_empty_queue, adm, adm_len, adm_minlen);
+    }
+    gather_first(G);
+    return admit_prefix(t, G, need_empty_queue, adm, adm_len, adm_minlen);
+  };
+
   while (true) {
     const int t = S.t;
     // (1) retire the jobs whose last token was processed at t-1
@@ -731,10 +750,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
         if (freew > 0) {
           const int kp = qcount;
           const int G = min(freew, kp);
-          if (G > 0 && !head_blocked()) {
-            gather_first(G);
-            admit_prefix(t, G, false, adm, adm_len, adm_minlen);
-          }
+          if (G > 0 && !head_blocked()) admit_first(t, G, false, adm, adm_len, adm_minlen);
         }
       }
     } else {  // ISJL
@@ -1028,8 +1044,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
               kv_block = true;
             } else {
               const int G = min(nie, kp);
-              gather_first(G);
-              const int na = admit_prefix(t, G, true, adm, adm_len, adm_minlen);
+              const int na = admit_first(t, G, true, adm, adm_len, adm_minlen);
               free_empty = nie - na;
               if (na < G) kv_block = true;
             }
@@ -1232,7 +1247,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
         e0 = t + readlane((int)dk[0], 0);
       };
       if constexpr (K >= 4) {
-        if (packed && N <= WAVE) sweep_body(std::integral_constant<int, 1>{});
+        // the packing goes through the gather buffer: only when it holds 64 words
+        if (packed && N <= WAVE && a.wave_words - a.off_stage >= WAVE)
+          sweep_body(std::integral_constant<int, 1>{});
         else sweep_body(std::integral_constant<int, K>{});
       } else {
         sweep_body(std::integral_constant<int, K>{});

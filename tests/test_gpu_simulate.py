@@ -309,3 +309,40 @@ def test_resume_fill_reading(dev):
     got, gs, gf = gpu_sim(dev, a, p, o, resume_fill=True, **kw)
     ref, rs, rf = oracle.simulate(a, p, o, schedule=True, flags=oracle.FLAG_RESUME_FILL, **kw)
     assert_same("resume lognormal sample", got, ref, gs, rs, gf, rf)
+
+
+def test_kv_budget_cuts_long_admission_batches(dev):
+    """Admission batches of more than 8 jobs under a KV budget that stops them at
+    every position around 8 (the small-slot kernels scan the first 8 alone):
+    offline and with releases, every policy."""
+    rng = np.random.default_rng(404)
+    for trial in range(6):
+        n, B = 180, int(rng.choice([40, 100, 200]))
+        a, p, o = workload.random_tables(rng, 24, n, 3, 12,
+                                         max_arrival=0 if trial % 2 == 0 else 50,
+                                         sorted_arrivals=True)
+        for M in (60, 100, 113, 140, 400):
+            for pol, al in (("isjl", 2), ("isjl", ALPHA_INF), ("ljf", ALPHA_INF),
+                            ("sjf", ALPHA_INF), ("fcfs", ALPHA_INF)):
+                ctx = f"kv cut {pol} alpha={al} B={B} M={M} trial={trial}"
+                check(dev, ctx, a, p, o, policy=pol, B=B, alpha=al, M_kv=M, cost_c=2,
+                      cost_tau=1)
+
+
+def test_many_slots_with_quiet_sweeps(dev):
+    """4 or more worker slots per lane (B > 128) with releases spaced so that the
+    machine often runs a few dozen jobs with nothing queued: the completions
+    before the next release are swept with the active slots packed through the
+    gather buffer (FCFS has one only for this).  Several instances per block, so
+    a pack that strayed past its wave's LDS would show up in a neighbour."""
+    rng = np.random.default_rng(2024)
+    for B in (200, 512, 1024):
+        for M in (0, 400):
+            a, p, o = workload.random_tables(rng, 12, 600, 3, 14, max_arrival=900,
+                                             sorted_arrivals=True)
+            for pol, al in (("fcfs", ALPHA_INF), ("sjf", ALPHA_INF), ("isjl", 3),
+                            ("isjl", ALPHA_INF), ("ljf", ALPHA_INF)):
+                ctx = f"quiet sweeps {pol} alpha={al} B={B} M={M}"
+                log(ctx)
+                check(dev, ctx, a, p, o, policy=pol, B=B, alpha=al, M_kv=M, cost_c=2,
+                      cost_tau=1)
