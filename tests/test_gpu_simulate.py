@@ -346,3 +346,17 @@ def test_many_slots_with_quiet_sweeps(dev):
                 log(ctx)
                 check(dev, ctx, a, p, o, policy=pol, B=B, alpha=al, M_kv=M, cost_c=2,
                       cost_tau=1)
+
+
+@pytest.mark.parametrize("policy,alpha", [("fcfs", ALPHA_INF), ("sjf", ALPHA_INF),
+                                          ("ljf", 30), ("isjl", 30), ("isjl", ALPHA_INF)])
+def test_unsorted_arrivals_many_jobs(dev, policy, alpha):
+    """The general variant (arrivals not in index order) at two bitmap words per
+    lane and up to 16 slots per lane, with and without a KV budget."""
+    rng = np.random.default_rng(zlib.crc32(f"unsorted-big:{policy}:{alpha}".encode()))
+    for n, B, M in ((4096, 1024, 0), (3000, 300, 20000), (2500, 150, 0)):
+        a, p, o = workload.random_tables(rng, 3, n, 40, 100, max_arrival=4000)
+        ctx = f"unsorted big {policy} alpha={alpha} n={n} B={B} M={M}"
+        log(ctx)
+        check(dev, ctx, a, p, o, policy=policy, B=B, alpha=alpha, M_kv=M, cost_c=5,
+              cost_tau=1)
