@@ -80,11 +80,13 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--alpha", default=None,
+                    help="sweep mode: a single fairness budget (an integer or 'inf')")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the per-alpha roofline lines of the fairness-budget sweep workload")
     ap.add_argument("--mode", default="simulate",
                     choices=["simulate", "copy", "decompose", "opt", "host", "profit",
-                             "gamma", "robust", "efficiency", "prefill"],
+                             "gamma", "robust", "efficiency", "prefill", "sweep"],
                     help="simulate: the benchmark line; copy: a plain device copy of known size "
                          "(calibrates the HBM byte counters); decompose / opt: time the other "
                          "two library calls (for profiles); host: host-buffer calls, "
@@ -93,7 +95,8 @@ def main() -> int:
                          "predicted sizes (pareto_65536x2000 and the guarantee on tiny "
                          "instances); efficiency: throughput and AEL of every policy on the "
                          "LMSYS-shaped workload; prefill: the prefill-at-admission variant "
-                         "of every policy on pareto_65536x2000")
+                         "of every policy on pareto_65536x2000; sweep: the fairness-budget "
+                         "sweep alone (--alpha to pick one budget, for counter runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the instances are "
@@ -124,6 +127,14 @@ def main() -> int:
         return time_efficiency(np, workload)
     if args.mode == "prefill":
         return time_prefill(torch, np, workload, fs, args)
+    if args.mode == "sweep":
+        alphas = None
+        if args.alpha is not None:
+            alphas = [workload.ALPHA_INF if args.alpha == "inf" else int(args.alpha)]
+        res = alpha_sweep(torch, np, workload, fs, torch.cuda.current_stream(),
+                          reps=max(1, args.steps), alphas=alphas)
+        print(json.dumps({"mode": "sweep", **res}))
+        return 0
     w = workload.WORKLOADS[args.workload]
     alpha = w.alphas[0]
     policy = "isjl"
@@ -204,7 +215,7 @@ def main() -> int:
     return 0
 
 
-def alpha_sweep(torch, np, workload, fs, stream, reps: int = 5) -> dict:
+def alpha_sweep(torch, np, workload, fs, stream, reps: int = 5, alphas=None) -> dict:
     """ISJL over the fairness-budget sweep workload (4,096 instances x 2,000 jobs,
     B = 128, M_kv = 262,144), one launch per alpha: instance-steps/s and the
     fraction of the ALU roofline, kernel time from HIP events (median of reps)."""
@@ -214,7 +225,7 @@ def alpha_sweep(torch, np, workload, fs, stream, reps: int = 5) -> dict:
     ta, tp, to = (torch.from_numpy(x).to("cuda:0") for x in (a, p, o))
     ops = algorithmic_ops(w.n_inst, w.n_jobs, w.B, "isjl", sorted_arrivals)
     rows = []
-    for al in w.alphas:
+    for al in (w.alphas if alphas is None else alphas):
         kw = dict(policy="isjl", B=w.B, alpha=al, M_kv=w.M_kv, cost_c=w.cost_c,
                   cost_tau=w.cost_tau)
         raw, _, _ = fs.simulate(ta, tp, to, **kw)
