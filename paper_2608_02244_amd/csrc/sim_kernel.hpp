@@ -444,8 +444,45 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
     return S.res + resv_len(pid(wv), plen(wv)) > M;
   };
 
-  // The first G queued ranks, in priority order, into STG[0..G).
+  // The first G queued ranks, in priority order, into STG[0..G).  Each lane
+  // writes its own word's ranks in turn; with up to 4 slots per lane, one bitmap
+  // word per lane and more than 8 ranks, lane L instead finds the rank at
+  // position c + L directly: the lane holding it by a binary search over the
+  // lanes' inclusive counts, then the right set bit of that lane's word.
   auto gather_first = [&](int G) {
+    if constexpr (K <= 4 && NW == 1) {
+      if (G > 8) {
+        const uint32_t x = pool.w[0];
+        const int cnt = __builtin_popcount(x);
+        const int incl = wave_scan_incl(cnt);
+        for (int c0 = 0; c0 < G; c0 += WAVE) {
+          const int P = c0 + lane;
+          int lo = 0;  // number of lanes whose count ends at or before P
+#pragma unroll
+          for (int step = WAVE / 2; step >= 1; step >>= 1) {
+            const int v = __shfl(incl, lo + step - 1);
+            if (v <= P) lo += step;
+          }
+          const int owner = lo < WAVE ? lo : WAVE - 1;
+          uint32_t w = (uint32_t)__shfl((int)x, owner);
+          int k = P - (__shfl(incl, owner) - __builtin_popcount(w));
+          // the k-th set bit of w (k < popcount(w) for every P < G)
+          int bit = 0;
+#pragma unroll
+          for (int half = 16; half >= 1; half >>= 1) {
+            const int c = __builtin_popcount(w & ((1u << half) - 1u));
+            if (k >= c) {
+              k -= c;
+              bit += half;
+              w >>= half;
+            }
+          }
+          if (P < G) STG[P] = (uint16_t)((owner << 5) + bit);
+        }
+        wave_lds_sync();
+        return;
+      }
+    }
     int gbase = 0;
 #pragma unroll
     for (int i = 0; i < NW; ++i) {
