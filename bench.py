@@ -382,9 +382,13 @@ def time_efficiency(np, workload) -> int:
     a, p, o = workload.generate("lmsys_shaped_256x2000")
     out = {"mode": "efficiency", "workload": "lmsys_shaped_256x2000"}
     ef.run_table(ef.gpu_simulate, a[:8], p[:8], o[:8], Bs=(16,))  # warm-up
-    for name, arr in (("poisson", a), ("offline", np.zeros_like(a))):
+    resume = lambda *x: ef.gpu_simulate(*x, resume_fill=True)  # noqa: E731
+    for name, arr, sim in (("poisson", a, ef.gpu_simulate), ("offline", np.zeros_like(a),
+                                                              ef.gpu_simulate),
+                           ("poisson_resume_fill", a, resume),
+                           ("offline_resume_fill", np.zeros_like(a), resume)):
         t0 = time.perf_counter()
-        tab = ef.run_table(ef.gpu_simulate, arr, p, o)
+        tab = ef.run_table(sim, arr, p, o)
         out[name] = {"seconds": time.perf_counter() - t0, "table": {str(B): r for B, r in
                                                                     tab.items()},
                      "markdown": ef.format_table(tab)}

@@ -30,15 +30,17 @@ def label(policy: str, alpha: Optional[int]) -> str:
     return policy.upper() if alpha is None else f"{policy.upper()}({alpha})"
 
 
-def gpu_simulate(a, p, o, policy: str, B: int, alpha: int, M_kv: int = 0):
-    """Every instance through the HIP library on cuda:0; metrics on the host."""
+def gpu_simulate(a, p, o, policy: str, B: int, alpha: int, M_kv: int = 0,
+                 resume_fill: bool = False):
+    """Every instance through the HIP library on cuda:0; metrics on the host
+    (``resume_fill``: ISJL's other reading of Phase TWO's stop)."""
     import torch
     from . import metrics_view, simulate
     dev = torch.device("cuda:0")
     ta, tp, to = (torch.from_numpy(np.ascontiguousarray(x, dtype=np.int32)).to(dev)
                   for x in (a, p, o))
     raw, _, _ = simulate(ta, tp, to, policy=policy, B=B, alpha=alpha, M_kv=M_kv, cost_c=0,
-                         cost_tau=1)
+                         cost_tau=1, resume_fill=resume_fill and policy == "isjl")
     return metrics_view(raw).copy()
 
 
