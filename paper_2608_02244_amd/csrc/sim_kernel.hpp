@@ -166,9 +166,11 @@ struct SimState {
 // progress): a job runs one step per output token, reserves prompt + output and
 // its footprint in the batch cost is prompt + progress; fairness stays on
 // progress.  The sweeps are off (completions are taken one event at a time).
-template <int POL, int K, int NW, bool GEN, bool ROB, bool PRE>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 : 1))) void simulate_kernel(SimArgs a) {
+// FILL: with the fill sweep (below), for up to 2 slots per lane.
+template <int POL, int K, int NW, bool GEN, bool ROB, bool PRE, bool FILL>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : (K <= 8 ? 3 : 1)))) void simulate_kernel(SimArgs a) {
   static_assert(!ROB || POL == POL_ISJL, "predicted sizes: ISJL only");
+  static_assert(!FILL || (K <= 2 && !ROB && !PRE && POL != POL_LJF), "fill sweep variants");
   extern __shared__ uint32_t lds_raw[];
   const int wib = threadIdx.x >> 6;
   const int64_t inst = (int64_t)blockIdx.x * (blockDim.x >> 6) + wib;
@@ -1097,6 +1099,429 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
       S.max_s = t;
     }
 
+    // Fill sweep (up to 2 slots per lane; FCFS, SJF, and ISJL in FILL with
+    // nothing planned; jobs queued).  Each coming completion admits the next
+    // jobs of the queue's strict prefix that fit the freed slots and the KV
+    // budget.  While no job admitted meanwhile completes, nothing is released
+    // and (ISJL) A_max stays within alpha at each completion, the admissions
+    // follow from counts: after the completions at the sorted positions <= p,
+    // the first
+    //   A(p) = min(G, free + p + 1, #{j : PQ_j <= M - res + RR_p})
+    // queued jobs are in (PQ_j: summed reservations of the queued jobs 0..j in
+    // priority order; RR_p: of the completed positions 0..p; A is
+    // non-decreasing), and queued job j starts at the completion of the first
+    // position with A(p) > j.  The spans are accounted in parallel as in the
+    // drain sweep, with the admitted jobs added to the suffix sums, up to the
+    // first completion, admitted job's completion, release or (ISJL, KV budget
+    // blocking an idle worker) alpha crossing that the counts do not decide;
+    // the event loop takes it from there.  The last group of completions is
+    // always left to the event loop, so every counted event has a job of the
+    // sorted set still active.
+    if constexpr (FILL) {
+      const int Qn = POL == POL_FCFS ? relk - head : qcount;
+      if (S.nact >= 2 && Qn > 0 && (POL != POL_ISJL || (mode == 0 && planned == 0))) {
+        int H = IDLE;  // next release
+        if (POL == POL_FCFS || !GEN) {
+          if (relk < n) {
+            if ((relk >> 6) != chunk) load_chunk(relk >> 6);
+            H = readlane(rel_t, relk & (WAVE - 1));
+          }
+        } else {
+          H = next_rel;
+        }
+        // taken when a few completions come before the first queued job could
+        // finish after being admitted at the first of them (ISJL: and before
+        // A_max surely exceeds alpha: some job started by max_s stays active)
+        const int r0 = POL == POL_FCFS ? head : pool.first();
+        int64_t lim0 = min((int64_t)H, (int64_t)S.min_end + plen(W[r0]));
+        if (POL == POL_ISJL) lim0 = min(lim0, (int64_t)S.max_s + alpha + 1);
+        int ahead = 0;
+#pragma unroll
+        for (int k = 0; k < K; ++k)
+          ahead += __builtin_popcountll(ballot(ws_end[k] != IDLE && (int64_t)ws_end[k] < lim0));
+        if (ahead >= 4) {
+          const int N = S.nact;
+          const int Gq = min(Qn, Beff);
+          constexpr int NS = K * WAVE;
+          // queued job j (register j / 64, lane j % 64) and sorted position q
+          // (lane q / K, register q % K); the shuffles run on every lane
+          auto at_job = [&](const int(&v)[K], int j) -> int {
+            if constexpr (K == 1) {
+              return __shfl(v[0], j & (WAVE - 1));
+            } else {
+              const int v0 = __shfl(v[0], j & (WAVE - 1)), v1 = __shfl(v[1], j & (WAVE - 1));
+              return (j >> 6) ? v1 : v0;
+            }
+          };
+          auto at_pos = [&](const int(&v)[K], int q) -> int {
+            if constexpr (K == 1) {
+              return __shfl(v[0], q & (WAVE - 1));
+            } else {
+              const int v0 = __shfl(v[0], (q >> 1) & (WAVE - 1));
+              const int v1 = __shfl(v[1], (q >> 1) & (WAVE - 1));
+              return (q & 1) ? v1 : v0;
+            }
+          };
+          auto at_pos_u = [&](const int(&v)[K], int q) -> int {  // q uniform
+            if constexpr (K == 1) {
+              return readlane(v[0], q);
+            } else {
+              const int v0 = readlane(v[0], q >> 1), v1 = readlane(v[1], q >> 1);
+              return (q & 1) ? v1 : v0;
+            }
+          };
+          // active jobs sorted by completion: end - t, progress t - start
+          uint32_t dk[K];
+          int dg[K];
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            const bool act = ws_end[k] != IDLE;
+            dk[k] = act ? (uint32_t)(ws_end[k] - t) : 0xFFFFFFFFu;
+            dg[k] = act ? t - ws_start[k] : 0;
+          }
+          reg_sort_payload<K>(dk, dg, lane);
+          int de[K];  // completion - t of each position (IDLE past N)
+#pragma unroll
+          for (int k = 0; k < K; ++k) de[k] = lane * K + k < N ? (int)dk[k] : IDLE;
+          const int e_up = __shfl_down(de[0], 1);  // first position of the next lane
+          // progress sum / max / min of the positions of the lanes above
+          int xs_g, xs_max, xs_min;
+          {
+            int lg = 0, lmx = -1, lmn = IDLE;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              if (lane * K + k < N) {
+                lg += dg[k];
+                lmx = max(lmx, dg[k]);
+                lmn = min(lmn, dg[k]);
+              }
+            }
+            const int incl = wave_scan_incl(lg);
+            xs_g = readlane(incl, WAVE - 1) - incl;
+            const int rmx = wave_scan_incl_max(__shfl(lmx, (WAVE - 1) - lane));
+            const int rmn = wave_scan_incl_min(__shfl(lmn, (WAVE - 1) - lane));
+            const int src = lane < WAVE - 1 ? (WAVE - 2) - lane : 0;
+            xs_max = __shfl(rmx, src);
+            xs_min = __shfl(rmn, src);
+            if (lane == WAVE - 1) {
+              xs_max = -1;
+              xs_min = IDLE;
+            }
+          }
+          // ISJL: completions before the first one after which A_max exceeds
+          // alpha, or (with a KV budget, which may block an idle worker) whose
+          // following span the alpha crossing may cut; fewer than 3 are left
+          // to the event loop
+          bool go = true;
+          if (POL == POL_ISJL) {
+            int lfail = IDLE, lcutq = IDLE;
+            int cg_max = xs_max;
+#pragma unroll
+            for (int k = K - 1; k >= 0; --k) {
+              const int q = lane * K + k;
+              const int e = de[k];
+              const int e_nx = (k + 1 < K) ? de[k + 1 < K ? k + 1 : k] : e_up;
+              if (q < N && (q + 1 >= N || e_nx > e)) {
+                if (q + 1 >= N || e + cg_max > alpha) lfail = q;
+                else if (M != 0 && alpha != IDLE && alpha + 1 - cg_max < e_nx) lcutq = q;
+              }
+              if (q < N) cg_max = max(cg_max, dg[k]);
+            }
+            const int qc = wave_min(lcutq);
+            const int qf = min(wave_min(lfail), qc == IDLE ? IDLE : qc + 1);
+            int lbelow = 0;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              const int q = lane * K + k;
+              const int e_nx = (k + 1 < K) ? de[k + 1 < K ? k + 1 : k] : e_up;
+              if (q < qf && e_nx > de[k]) lbelow++;
+            }
+            go = wave_sum(lbelow) >= 3;
+          }
+          if (go) {
+          if (POL != POL_FCFS) gather_first(Gq);
+          // queued jobs: length and summed reservations in priority order
+          int qlen[K], pq[K];
+          {
+            int carry = 0;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              const int j = k * WAVE + lane;
+              int L = 0;
+              if (j < Gq) L = plen(W[POL == POL_FCFS ? head + j : (int)STG[j]]);
+              qlen[k] = L;
+              const int inc = wave_scan_incl(L);
+              pq[k] = j < Gq ? carry + inc : IDLE;
+              carry += readlane(inc, WAVE - 1);
+            }
+          }
+          // A(q): queued jobs admitted once the positions <= q have completed
+          int ap[K];
+          {
+            int rr[K], run = 0;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              if (lane * K + k < N) run += de[k] + dg[k];  // lengths (= reservations)
+              rr[k] = run;
+            }
+            const int rbase = wave_scan_incl(run) - run;
+            const int64_t bud0 = (int64_t)M - S.res;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              const int q = lane * K + k;
+              int v = min(Gq, Beff - N + q + 1);
+              if (M != 0) {
+                const int64_t b = bud0 + rbase + rr[k];
+                const int bb = b < 0 ? -1 : (b >= (int64_t)IDLE ? IDLE - 1 : (int)b);
+                int lo = 0;  // queued jobs whose summed reservations fit
+#pragma unroll
+                for (int step = NS; step >= 1; step >>= 1) {
+                  const int x = at_job(pq, min(lo + step, NS) - 1);
+                  if (lo + step <= NS && x <= bb) lo += step;
+                }
+                v = min(v, lo);
+              }
+              ap[k] = q < N ? v : IDLE;
+            }
+          }
+          // start of queued job j relative to t (IDLE: not admitted at these
+          // positions), the earliest completion among jobs 0..j and their
+          // summed starts
+          int sg[K], pm[K], sa[K];
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            const int j = k * WAVE + lane;
+            int lo = 0;  // positions with A <= j
+#pragma unroll
+            for (int step = NS; step >= 1; step >>= 1) {
+              const int x = at_pos(ap, min(lo + step, NS) - 1);
+              if (lo + step <= NS && x <= j) lo += step;
+            }
+            const int e = at_pos(de, min(lo, NS - 1));
+            sg[k] = lo < N ? e : IDLE;
+          }
+          {
+            int cm = IDLE, cs = 0;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              const int im = wave_scan_incl_min(sg[k] == IDLE ? IDLE : sg[k] + qlen[k]);
+              pm[k] = min(cm, im);
+              cm = min(cm, readlane(im, WAVE - 1));
+              const int is = wave_scan_incl(sg[k] == IDLE ? 0 : sg[k]);
+              sa[k] = cs + is;
+              cs += readlane(is, WAVE - 1);
+            }
+          }
+          const int Hr = H == IDLE ? IDLE : H - t;
+          // Which completions the counts decide: the event at group end q is
+          // taken if nothing is released by then, no admitted job has completed
+          // by then and (ISJL) A_max after it is within alpha; the span after it
+          // ends early (lim) at an admitted job's completion or, with an idle
+          // worker blocked by the KV budget, at the alpha crossing.
+          int lbad = IDLE, lcut = IDLE, lim[K];
+          uint32_t gem = 0u;
+          {
+            int cg_max = xs_max;
+#pragma unroll
+            for (int k = K - 1; k >= 0; --k) {
+              const int q = lane * K + k;
+              const bool vq = q < N;
+              const int e = de[k];
+              const int e_nx = (k + 1 < K) ? de[k + 1 < K ? k + 1 : k] : e_up;
+              const bool ge = vq && (q + 1 >= N || e_nx > e);
+              const int A = vq ? ap[k] : 0;
+              const int pmA = at_job(pm, max(A - 1, 0));
+              lim[k] = IDLE;
+              if (ge) {
+                gem |= 1u << k;
+                bool ok = q + 1 < N && e < Hr && (A == 0 || pmA > e);
+                if (POL == POL_ISJL) ok = ok && e + cg_max <= alpha;
+                if (!ok) {
+                  lbad = q;
+                } else {
+                  int cut = A > 0 ? pmA : IDLE;
+                  if (POL == POL_ISJL && alpha != IDLE && N - 1 - q + A < Beff && A < Qn)
+                    cut = min(cut, alpha + 1 - cg_max);
+                  if (cut < e_nx) lcut = q;
+                  lim[k] = min(min(e_nx, Hr), cut);
+                }
+              }
+              if (vq) cg_max = max(cg_max, dg[k]);
+            }
+          }
+          const int pe = wave_min(lbad), pc = wave_min(lcut);
+          int p_m;
+          {
+            int lpm = -1;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              const int q = lane * K + k;
+              if (((gem >> k) & 1u) && q < pe && q <= pc) lpm = q;
+            }
+            p_m = wave_max(lpm);
+          }
+          const int e_first = readlane(de[0], 0);
+          if (POL == POL_ISJL && kv_block && alpha != IDLE && S.min_s + alpha + 1 - t < e_first)
+            p_m = -1;  // the crossing comes first
+          int tau_rel;
+          if (p_m >= 0) {
+            tau_rel = at_pos_u(lim, p_m);
+          } else {
+            tau_rel = min(e_first, Hr);
+            if (POL == POL_ISJL && kv_block && alpha != IDLE)
+              tau_rel = min(tau_rel, S.min_s + alpha + 1 - t);
+          }
+          const int A_m = p_m >= 0 ? at_pos_u(ap, p_m) : 0;
+          // spans after each counted event, with the jobs at the positions
+          // above and the admitted jobs 0..A-1
+          int64_t lE = 0, lSM = 0, lSSM = 0, lX = 0, lP = 0;
+          int lU = 0, lmx = 0, lma = 0;
+          {
+            int cg = xs_g, cg_max = xs_max, cg_min = xs_min;
+#pragma unroll
+            for (int k = K - 1; k >= 0; --k) {
+              const int q = lane * K + k;
+              const bool vq = q < N;
+              const int e = de[k];
+              const int e_nx = (k + 1 < K) ? de[k + 1 < K ? k + 1 : k] : e_up;
+              const int A = vq ? ap[k] : 0;
+              const int saA = at_job(sa, max(A - 1, 0)), sgA = at_job(sg, max(A - 1, 0));
+              if (((gem >> k) & 1u) && q <= p_m) {
+                const int Er = q == p_m ? tau_rel : e_nx;
+                const int64_t D = (int64_t)(Er - e);
+                const int64_t so = N - 1 - q, s = so + A;
+                const int min_s = t - cg_max;
+                const int max_s = A > 0 ? t + sgA : t - cg_min;
+                const int64_t sum_s = s * (int64_t)t - cg + (A > 0 ? saA : 0);
+                const int64_t m0 = (int64_t)(t + e - min_s) + 1;
+                const int64_t sm = D * m0 + D * (D - 1) / 2;
+                lE += D * (sum_s - s * (int64_t)min_s);
+                lSM += sm;
+                lSSM += s * sm;
+                const int ext = max_s - min_s;
+                lX += D * ext;
+                if (ext > alpha) lU += (int)D;
+                lP = max(lP, s * (int64_t)(t + Er) - sum_s);
+                lmx = max(lmx, ext);
+                lma = max(lma, (int)s);
+              }
+              if (vq) {
+                cg += dg[k];
+                cg_max = max(cg_max, dg[k]);
+                cg_min = min(cg_min, dg[k]);
+              }
+            }
+          }
+          // span [t, first event): the jobs active now
+          {
+            const int64_t D = (int64_t)(p_m >= 0 ? e_first : tau_rel), s = N;
+            const int64_t m0 = (int64_t)(t - S.min_s) + 1;
+            const int64_t sm = D * m0 + D * (D - 1) / 2;
+            if (lane == 0) {
+              lE += D * (S.sum_s - s * (int64_t)S.min_s);
+              lSM += sm;
+              lSSM += s * sm;
+              const int ext = S.max_s - S.min_s;
+              lX += D * ext;
+              if (ext > alpha) lU += (int)D;
+              lP = max(lP, s * (int64_t)(t + D) - S.sum_s);
+              lmx = max(lmx, ext);
+              lma = max(lma, N);
+            }
+          }
+          const int64_t span = (int64_t)tau_rel;
+          const int64_t sSM = wave_sum64(lSM), sSSM = wave_sum64(lSSM);
+          acc_E += wave_sum64(lE);
+          acc_C += a.c * span + a.tau * sSSM;
+          acc_W += a.c * span + a.tau * sSM;
+          acc_ext += wave_sum64(lX);
+          acc_busy += span;
+          acc_unfair += wave_sum(lU);
+          acc_peak = max(acc_peak, wave_max64(lP));
+          acc_maxext = max(acc_maxext, wave_max(lmx));
+          acc_maxact = max(acc_maxact, wave_max(lma));
+          // completions of the admitted jobs
+          {
+            int lsc = 0;
+#pragma unroll
+            for (int k = 0; k < K; ++k)
+              if (k * WAVE + lane < A_m) lsc += sg[k] + qlen[k];
+            S.sum_comp += (int64_t)A_m * t + wave_sum(lsc);
+          }
+          // retire every job done by tau, then seat the admitted ones that are
+          // still running
+          const int tau = t + tau_rel;
+          int lret = 0;
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            if (ws_end[k] <= tau) {
+              lret++;
+              ws_end[k] = IDLE;
+              ws_start[k] = IDLE;
+            }
+          }
+          if (A_m > 0) {
+            int base = 0;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              const bool idle = valid[k] && ws_end[k] == IDLE;
+              const uint64_t bm = ballot(idle);
+              const int idx = base + mbcnt(bm);
+              const int jc = min(idx, A_m - 1);
+              const int s_rel = at_job(sg, jc), L = at_job(qlen, jc);
+              if (idle && idx < A_m) {
+                const int rk = POL == POL_FCFS ? head + idx : (int)STG[idx];
+                const int st = t + s_rel;
+                emit(pid(W[rk]), st, L);
+                if (st + L > tau) {
+                  ws_start[k] = st;
+                  ws_end[k] = st + L;
+                } else {
+                  lret++;
+                }
+              }
+              base += __builtin_popcountll(bm);
+            }
+            if (POL == POL_FCFS) {
+              head += A_m;
+            } else {
+              pool.clear_upto(STG[A_m - 1], lane);
+              qcount -= A_m;
+            }
+          }
+          S.ndone += wave_sum(lret);
+          {
+            int cnt = 0, lres = 0, mn = IDLE, mx = -1, me = IDLE;
+            int64_t ss = 0;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+              if (ws_end[k] != IDLE) {
+                cnt++;
+                lres += ws_end[k] - ws_start[k];
+                ss += ws_start[k];
+                mn = min(mn, ws_start[k]);
+                mx = max(mx, ws_start[k]);
+                me = min(me, ws_end[k]);
+              }
+            }
+            S.nact = wave_sum(cnt);
+            S.res = wave_sum(lres);
+            S.sum_s = wave_sum64(ss);
+            S.min_s = S.nact > 0 ? wave_min(mn) : IDLE;
+            S.max_s = S.nact > 0 ? wave_max(mx) : -1;
+            S.min_end = wave_min(me);
+          }
+          S.t = tau;
+          if (++iter > iter_max) {
+            failed = true;
+            break;
+          }
+          continue;
+          }
+        }
+      }
+    }
+
     // Drain sweep.  LJF between batches and ISJL in DRAIN admit nothing through
     // Phase TWO, and a planned ISJL job can start only at a step where
     // A_max(t) <= alpha, which (A_max grows between completions) can first hold
@@ -1444,23 +1869,38 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(K <= 8 ? 3 
   }
 }
 
+// The fill sweep serves FCFS and SJF with up to 2 slots per lane, and ISJL there
+// when alpha is at least the length limit (A_max, below every length, never
+// exceeds it).  With a finite budget ISJL's completions mostly meet the guard
+// one at a time, and its event loop runs faster without the sweep's code.
 template <int POL, bool ROB = false, bool PRE = false>
 hipError_t launch_sim(const SimArgs& a, int K, int NW, bool general, int wpb, size_t lds,
                       hipStream_t s) {
   const int64_t blocks = (a.n_inst + wpb - 1) / wpb;
   dim3 grid((unsigned)blocks), block((unsigned)(wpb * WAVE));
-#define FS_LAUNCH(KK, NN, GG)                                                        \
-  if (K == KK && NW == NN && general == GG) {                                        \
-    hipLaunchKernelGGL((simulate_kernel<POL, KK, NN, GG, ROB, PRE>), grid, block, lds, s, a);  \
-    return hipGetLastError();                                                        \
+  constexpr bool FILL_OK = !ROB && !PRE && POL != POL_LJF;
+  constexpr bool FILL_ALWAYS = FILL_OK && POL != POL_ISJL;
+  const bool fill = FILL_OK && K <= 2 && (FILL_ALWAYS || a.alpha >= (int)LEN_LIMIT);
+#define FS_LAUNCH(KK, NN, GG, FF)                                                      \
+  if (K == KK && NW == NN && general == GG && fill == FF) {                            \
+    hipLaunchKernelGGL((simulate_kernel<POL, KK, NN, GG, ROB, PRE, FF>), grid, block, lds, s, \
+                       a);                                                             \
+    return hipGetLastError();                                                          \
   }
-#define FS_LAUNCH_K(KK) \
-  FS_LAUNCH(KK, 1, false) FS_LAUNCH(KK, 2, false) FS_LAUNCH(KK, 1, true) FS_LAUNCH(KK, 2, true)
-  FS_LAUNCH_K(1)
-  FS_LAUNCH_K(2)
-  FS_LAUNCH_K(4)
-  FS_LAUNCH_K(8)
-  FS_LAUNCH_K(16)
+#define FS_LAUNCH_K(KK, FF)                                                         \
+  FS_LAUNCH(KK, 1, false, FF) FS_LAUNCH(KK, 2, false, FF) FS_LAUNCH(KK, 1, true, FF) \
+  FS_LAUNCH(KK, 2, true, FF)
+  if constexpr (FILL_OK) {
+    FS_LAUNCH_K(1, true)
+    FS_LAUNCH_K(2, true)
+  }
+  if constexpr (!FILL_ALWAYS) {
+    FS_LAUNCH_K(1, false)
+    FS_LAUNCH_K(2, false)
+  }
+  FS_LAUNCH_K(4, false)
+  FS_LAUNCH_K(8, false)
+  FS_LAUNCH_K(16, false)
 #undef FS_LAUNCH_K
 #undef FS_LAUNCH
   return hipErrorInvalidValue;

@@ -360,3 +360,24 @@ def test_unsorted_arrivals_many_jobs(dev, policy, alpha):
         log(ctx)
         check(dev, ctx, a, p, o, policy=policy, B=B, alpha=alpha, M_kv=M, cost_c=5,
               cost_tau=1)
+
+
+@pytest.mark.parametrize("policy,alpha", [("fcfs", ALPHA_INF), ("sjf", ALPHA_INF),
+                                          ("isjl", ALPHA_INF), ("isjl", 1 << 20),
+                                          ("isjl", (1 << 20) - 1)])
+def test_fill_sweep_queued_completions(dev, policy, alpha):
+    """Up to 2 slots per lane with a long queue: FCFS, SJF and ISJL with alpha at
+    least the length limit take runs of completions at once, each admitting the
+    next jobs of the queue (alpha just below the limit takes the variant
+    without it).  KV budgets from none to binding, all released at once,
+    releases through the run (in index order and not), and B from 4 to 128."""
+    rng = np.random.default_rng(zlib.crc32(f"fill:{policy}:{alpha}".encode()))
+    for n, B, M, arr in ((500, 4, 0, 0), (2000, 128, 0, 0), (2000, 100, 6000, 0),
+                         (1500, 64, 2500, 0), (2000, 128, 9000, 3000), (900, 37, 1500, 20000),
+                         (2000, 128, 0, -6000), (1200, 90, 4000, -2000)):
+        a, p, o = workload.random_tables(rng, 4, n, 60, 200, max_arrival=abs(arr),
+                                         sorted_arrivals=arr > 0)
+        ctx = f"fill sweep {policy} alpha={alpha} n={n} B={B} M={M} arrivals={arr}"
+        log(ctx)
+        check(dev, ctx, a, p, o, policy=policy, B=B, alpha=alpha, M_kv=M, cost_c=3,
+              cost_tau=2)
