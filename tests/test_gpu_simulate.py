@@ -370,11 +370,13 @@ def test_fill_sweep_queued_completions(dev, policy, alpha):
     least the length limit take runs of completions at once, each admitting the
     next jobs of the queue (alpha just below the limit takes the variant
     without it).  KV budgets from none to binding, all released at once,
-    releases through the run (in index order and not), and B from 4 to 128."""
+    releases through the run (in index order and not), B from 4 to 128 and one or
+    two job-bitmap words per lane."""
     rng = np.random.default_rng(zlib.crc32(f"fill:{policy}:{alpha}".encode()))
     for n, B, M, arr in ((500, 4, 0, 0), (2000, 128, 0, 0), (2000, 100, 6000, 0),
                          (1500, 64, 2500, 0), (2000, 128, 9000, 3000), (900, 37, 1500, 20000),
-                         (2000, 128, 0, -6000), (1200, 90, 4000, -2000)):
+                         (2000, 128, 0, -6000), (1200, 90, 4000, -2000), (3000, 120, 5000, 0),
+                         (4096, 64, 0, 8000)):
         a, p, o = workload.random_tables(rng, 4, n, 60, 200, max_arrival=abs(arr),
                                          sorted_arrivals=arr > 0)
         ctx = f"fill sweep {policy} alpha={alpha} n={n} B={B} M={M} arrivals={arr}"
