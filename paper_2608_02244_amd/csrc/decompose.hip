@@ -219,7 +219,10 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
   int pmin = 0, pmax = -1;             // first / last of their start events
   int cnt_last = 0;                    // |S| at the last group end
   int g_nst = 0, gfirst = -1, glast = -1;  // starts of the open group (before this chunk)
-  int64_t lE = 0, lC = 0, lW = 0, lX = 0, lB = 0, lU = 0, lP = 0;
+  // per lane: E, all span lengths, busy span lengths, sum of the largest
+  // footprint and of |S| times it (C and W take c and tau once at the end),
+  // extent, unfair steps, peak KV
+  int64_t lE = 0, lD = 0, lB = 0, lSM = 0, lSSM = 0, lX = 0, lU = 0, lP = 0;
   int lXm = 0, lAm = 0;
   bool lcap = false, lkv = false, lunf = false;
   // idle steps before the first event
@@ -257,10 +260,10 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
     const int len = valid ? LEN[key & 0xFFFu] : 0;
     const int sj = is_start ? t : t - len;  // the job's start
     const int cnt_p = c_cnt + wave_scan_incl(is_start ? 1 : (is_end ? -1 : 0));
-    const int64_t sum_p =
-        c_sum + wave_scan_incl64(is_start ? (int64_t)sj : (is_end ? -(int64_t)sj : 0));
-    const int64_t res_p =
-        c_res + wave_scan_incl64(is_start ? (int64_t)len : (is_end ? -(int64_t)len : 0));
+    // within a chunk the deltas sum to less than 64 x 2^20 in magnitude (times
+    // < 2^19, lengths < 2^20): 32-bit scans on top of the 64-bit carries
+    const int64_t sum_p = c_sum + (int64_t)wave_scan_incl(is_start ? sj : (is_end ? -sj : 0));
+    const int64_t res_p = c_res + (int64_t)wave_scan_incl(is_start ? len : (is_end ? -len : 0));
     int t_next = __shfl_down(t, 1);
     if (lane == WAVE - 1) t_next = base + WAVE < NE ? (int)(EV[base + WAVE] >> 13) : t;
     const bool last = p == NE - 1;
@@ -431,16 +434,14 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
     // event time; the last event has none)
     if (gend && !last) {
       const int64_t D = (int64_t)(t_next - t);
-      if (cnt_p == 0) {
-        lC += a.c * D;
-        lW += a.c * D;
-      } else {
+      lD += D;
+      if (cnt_p != 0) {
         const int64_t s = cnt_p;
         const int64_t m0 = (int64_t)(t - gmin) + 1;
         const int64_t sm = D * m0 + D * (D - 1) / 2;
         lE += D * (sum_p - s * (int64_t)gmin);
-        lC += a.c * D + a.tau * s * sm;
-        lW += a.c * D + a.tau * sm;
+        lSM += sm;
+        lSSM += s * sm;
         const int ext = gmax - gmin;
         lX += D * ext;
         lB += D;
@@ -460,8 +461,9 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
     c_res = readlane64(res_p, 63);
   }
   const int64_t acc_E = wave_sum64(lE);
-  const int64_t acc_C = c0 + wave_sum64(lC);
-  const int64_t acc_W = c0 + wave_sum64(lW);
+  const int64_t sD = wave_sum64(lD);
+  const int64_t acc_C = c0 + a.c * sD + a.tau * wave_sum64(lSSM);
+  const int64_t acc_W = c0 + a.c * sD + a.tau * wave_sum64(lSM);
   const int64_t acc_ext = wave_sum64(lX);
   const int64_t acc_busy = wave_sum64(lB);
   const int64_t acc_unf = wave_sum64(lU);
