@@ -3,7 +3,9 @@
 Integers must match exactly: every metric of every instance and the start and
 finish step of every job.  Small cases cover every policy, ragged sizes,
 releases (sorted and unsorted), KV budgets, alpha = 0 / infinity, B = 1 /
-unlimited and the kernel's size limits.  The named workloads run at full size
+unlimited, the kernel's size limits and the fill sweep (runs of completions
+admitting queued jobs, FCFS / SJF / ISJL at alpha >= 2^20 with up to 128
+workers).  The named workloads run at full size
 in the launch configuration the benchmark times; there the oracle checks
 sampled instances and identities that hold at any size check all of them.
 """
