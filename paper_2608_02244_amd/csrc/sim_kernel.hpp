@@ -391,7 +391,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
   S.sum_comp = 0;
   S.G = -IDLE;
   S.sp = 0;
-  int64_t acc_E = 0, acc_C = 0, acc_W = 0, acc_ext = 0, acc_busy = 0, acc_peak = 0, acc_unfair = 0;
+  // C = c T + tau sum_t |S_t| m_t and W = c T + tau sum_t m_t (m_t: the largest
+  // footprint at step t, 0 when idle): c and tau are applied once at the end
+  // (every step 0 .. T-1 is accounted exactly once)
+  int64_t acc_E = 0, acc_SM = 0, acc_SSM = 0, acc_ext = 0, acc_busy = 0, acc_peak = 0,
+          acc_unfair = 0;
   int acc_maxext = 0, acc_maxact = 0;
   int32_t* st_out = a.start ? a.start + row : nullptr;
   int32_t* fi_out = a.finish ? a.finish + row : nullptr;
@@ -1432,8 +1436,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
           const int64_t span = (int64_t)tau_rel;
           const int64_t sSM = wave_sum64(lSM), sSSM = wave_sum64(lSSM);
           acc_E += wave_sum64(lE);
-          acc_C += a.c * span + a.tau * sSSM;
-          acc_W += a.c * span + a.tau * sSM;
+          acc_SM += sSM;
+          acc_SSM += sSSM;
           acc_ext += wave_sum64(lX);
           acc_busy += span;
           acc_unfair += wave_sum(lU);
@@ -1737,8 +1741,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
       const int64_t span = (int64_t)(tau_end - t);
       const int64_t sSM = wave_sum64(lSM), sSSM = wave_sum64(lSSM);
       acc_E += wave_sum64(lE);
-      acc_C += a.c * span + a.tau * sSSM;
-      acc_W += a.c * span + a.tau * sSM;
+      acc_SM += sSM;
+      acc_SSM += sSSM;
       acc_ext += wave_sum64(lX);
       acc_busy += span;
       acc_unfair += wave_sum(lU);
@@ -1812,10 +1816,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
 
     // (6) account steps t .. tn-1 (Section 5)
     const int64_t D = (int64_t)(tn - t);
-    if (S.nact == 0) {
-      acc_C += a.c * D;
-      acc_W += a.c * D;
-    } else {
+    if (S.nact != 0) {
       const int64_t s = S.nact;
       // largest footprint at step t (it grows by one per step of the span) and
       // the span's externality: each active job pays the largest footprint
@@ -1830,8 +1831,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
       }
       const int64_t sm = D * m0 + D * (D - 1) / 2;
       acc_E += D * xe;
-      acc_C += a.c * D + a.tau * s * sm;
-      acc_W += a.c * D + a.tau * sm;
+      acc_SM += sm;
+      acc_SSM += s * sm;
       const int ext = S.max_s - S.min_s;
       acc_ext += D * ext;
       acc_busy += D;
@@ -1855,8 +1856,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
     m.O = osum;
     m.Q = qsum;
     m.E = acc_E;
-    m.C = acc_C;
-    m.W = acc_W;
+    m.C = a.c * (int64_t)S.t + a.tau * acc_SSM;
+    m.W = a.c * (int64_t)S.t + a.tau * acc_SM;
     m.sum_completion = S.sum_comp;
     m.sum_latency = S.sum_comp - rsum;
     m.sum_extent = acc_ext;
