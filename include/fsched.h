@@ -34,6 +34,13 @@
  *     the results are back in host memory.
  *   - The caller owns every buffer.  The library keeps no pointer after the
  *     call (host mode) or after the stream passes the call (device mode).
+ *   - fsched_simulate, fsched_simulate_robust and fsched_bruteforce_opt (every
+ *     policy but FCFS) also take a scratch table of 2 bytes per job (rows
+ *     rounded up to 64 jobs) on `stream`, from a memory pool the library creates
+ *     once per device and keeps for the process: freed on the stream after the
+ *     call's kernels, it stays in the pool for the next call (else the
+ *     device's default pool is used).  If neither can supply it the call
+ *     returns FSCHED_ENOMEM before enqueuing any kernel.
  *   - Return codes are FSCHED_OK or a negative FSCHED_E* code; outputs are
  *     undefined on error.  Argument errors (null pointers, bad sizes or
  *     parameters) are detected before any work is enqueued.  In device mode the

@@ -5,6 +5,7 @@
 #include <cstdint>
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 
 #include "fsched.h"
 #include "sim_common.hpp"
@@ -88,6 +89,39 @@ struct Staging {
   }
 };
 
+// Pool of the rank scratch (2 bytes per job) of the current device, created
+// once: allocations are stream-ordered, and what a call frees stays in the pool
+// (release threshold: never) so that repeated calls allocate nothing new.
+// Null when the device cannot make one.
+hipMemPool_t rank_pool() {
+  constexpr int kMaxDev = 64;
+  static std::mutex mu;
+  static hipMemPool_t pools[kMaxDev] = {};
+  static bool tried[kMaxDev] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> g(mu);
+  if (!tried[dev]) {
+    tried[dev] = true;
+    hipMemPoolProps props;
+    std::memset(&props, 0, sizeof(props));
+    props.allocType = hipMemAllocationTypePinned;
+    props.location.type = hipMemLocationTypeDevice;
+    props.location.id = dev;
+    hipMemPool_t pool = nullptr;
+    if (hipMemPoolCreate(&pool, &props) == hipSuccess) {
+      uint64_t keep = UINT64_MAX;
+      (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+      pools[dev] = pool;
+    }
+    (void)hipGetLastError();
+  }
+  return pools[dev];
+}
+
 int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int32_t* arrival,
                     const int32_t* prompt, const int32_t* output, fsched_metrics* out,
                     int64_t* out_T, int32_t* start, int32_t* finish, hipStream_t s,
@@ -129,8 +163,29 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
   a.out_T = out_T;
   a.start = start;
   a.finish = finish;
+  // rank table of the release chunks (not FCFS, whose order is the arrival
+  // order): from the library's pool, else from the device's default pool
+  a.rank_stride = (n + 63) & ~63;
+  a.rank = nullptr;
+  if (p->policy != FSCHED_FCFS) {
+    const size_t bytes = (size_t)n_inst * (size_t)a.rank_stride * 2;
+    hipMemPool_t pool = rank_pool();
+    void* r = nullptr;
+    hipError_t e = pool ? hipMallocFromPoolAsync(&r, bytes, pool, s) : hipErrorNotSupported;
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      r = nullptr;
+      e = hipMallocAsync(&r, bytes, s);
+    }
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return FSCHED_ENOMEM;
+    }
+    a.rank = (uint16_t*)r;
+  }
 
-  for (int general = 0; general < 2; ++general) {
+  hipError_t err = hipSuccess;
+  for (int general = 0; general < 2 && err == hipSuccess; ++general) {
     fs::SimArgs b = a;
     b.off_arr = NP;
     b.off_q = NP + (general ? NP : 0);
@@ -165,8 +220,10 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
                 : fs::launch_sim_sjf(b, K, NW, general, wpb, lds, s);
         break;
     }
-    if (e != hipSuccess) return hip_fail(e);
+    err = e;
   }
+  if (a.rank && hipFreeAsync(a.rank, s) != hipSuccess) (void)hipGetLastError();
+  if (err != hipSuccess) return hip_fail(err);
   return FSCHED_OK;
 }
 

@@ -40,6 +40,12 @@ struct SimArgs {
   int64_t* out_T;       // when non-null: only the makespan (or marker) per instance
   int32_t* start;
   int32_t* finish;
+  // Scratch: rank of every job in the priority order, written by the
+  // sorted-arrival kernel once it has sorted and read back at each release
+  // chunk (rows of rank_stride entries, a multiple of 64 so that no 128-byte
+  // line is shared by two instances).  Required for every policy but FCFS.
+  uint16_t* rank;
+  int32_t rank_stride;
 };
 
 // Chooses and launches the kernel instantiation for one policy.  `general`

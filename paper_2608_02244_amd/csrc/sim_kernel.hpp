@@ -323,6 +323,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
       default: wave_bitonic_sort(W, NP, lane); break;
     }
     wave_lds_sync();
+    // sorted-arrival kernel: each job's rank goes to the rank table for the
+    // release chunks (only this wave touches its row)
+    uint16_t* RKw = (!GEN && POL != POL_FCFS) ? a.rank + inst * (int64_t)a.rank_stride : nullptr;
     for (int r = lane; r < n; r += WAVE) {
       uint32_t key = W[r];
       int id = (int)(key & 0xFFFu);
@@ -332,7 +335,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
       else len = (uint32_t)(PRE ? O[id] : P[id] + O[id]);
       W[r] = (len << 12) | (uint32_t)id;
       if (GEN) ARR[r] = A[id];
+      else if (RKw) RKw[id] = (uint16_t)r;
     }
+    if (RKw) __threadfence_block();  // the stores complete before the row is read
   }
   wave_lds_sync();
 
@@ -403,7 +408,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
   int iter = 0;
   bool failed = false;
 
-  // Load release chunk `c` (64 consecutive jobs in arrival order).
+  // rank of each job in the priority order (sorted-arrival kernel, not FCFS)
+  const uint16_t* RK =
+      (!GEN && POL != POL_FCFS) ? a.rank + inst * (int64_t)a.rank_stride : nullptr;
+  // Load release chunk `c` (64 consecutive jobs in arrival order; the general
+  // variant releases through ARR and loads chunks only under FCFS).
   auto load_chunk = [&](int c) {
     int j = c * WAVE + lane;
     rel_t = IDLE;
@@ -412,21 +421,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
       if (j < n) rel_t = GEN ? ARR[j] : A[j];
       rel_r = j;
     } else if (j < n) {
-      // rank of job j: position of its priority key in W (binary search)
       rel_t = A[j];
-      uint32_t len = (uint32_t)((PRE ? 0 : P[j]) + (ROB ? U[j] : O[j]));
-      uint32_t key;
-      if (POL == POL_SJF) key = (len << 12) | (uint32_t)j;
-      else key = ((LMASK - len) << 12) | (uint32_t)j;
-      int lo = 0, hi = n;  // first rank whose key >= key
-      while (lo < hi) {
-        int mid = (lo + hi) >> 1;
-        uint32_t wv = W[mid];
-        uint32_t kv = (POL == POL_SJF) ? wv : (((LMASK - (wv >> 12)) << 12) | (wv & 0xFFFu));
-        if (kv < key) lo = mid + 1;
-        else hi = mid;
-      }
-      rel_r = lo;
+      rel_r = RK[j];
     }
     chunk = c;
   };

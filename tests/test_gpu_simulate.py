@@ -385,3 +385,30 @@ def test_fill_sweep_queued_completions(dev, policy, alpha):
         log(ctx)
         check(dev, ctx, a, p, o, policy=policy, B=B, alpha=alpha, M_kv=M, cost_c=3,
               cost_tau=2)
+
+
+def test_rank_scratch_reuse_across_calls_and_streams(dev):
+    """Every policy but FCFS takes its rank table from the library's stream-ordered
+    pool: back-to-back calls of different sizes on a side stream (no host sync in
+    between, the earlier tables freed on the stream) each match the oracle."""
+    import torch
+    rng = np.random.default_rng(99)
+    side = torch.cuda.Stream()
+    jobs = []
+    for n_inst, n, B, pol, al in ((40, 700, 64, "isjl", 9), (7, 2000, 128, "sjf", ALPHA_INF),
+                                  (25, 300, 16, "ljf", 5), (3, 4096, 300, "isjl", ALPHA_INF)):
+        a, p, o = workload.random_tables(rng, n_inst, n, 30, 90, max_arrival=3 * n,
+                                         sorted_arrivals=True)
+        jobs.append((a, p, o, dict(policy=pol, B=B, alpha=al, M_kv=5000, cost_c=2, cost_tau=1)))
+    outs = []
+    with torch.cuda.stream(side):
+        for a, p, o, kw in jobs:
+            ts = [torch.from_numpy(x).to(dev, non_blocking=False) for x in (a, p, o)]
+            raw, st, fi = fs.simulate(*ts, schedule=True, **kw)
+            outs.append((ts, raw, st, fi))
+    side.synchronize()
+    for (a, p, o, kw), (_, raw, st, fi) in zip(jobs, outs):
+        ctx = f"rank scratch reuse {kw}"
+        log(ctx)
+        ref, rs, rf = oracle.simulate(a, p, o, schedule=True, **kw)
+        assert_same(ctx, fs.metrics_view(raw), ref, st.cpu().numpy(), rs, fi.cpu().numpy(), rf)
