@@ -245,6 +245,13 @@ int fsched_abi_version(void);
 /* The hipError_t of the last FSCHED_EDEVICE return on the calling thread. */
 int fsched_last_hip_error(void);
 
+/* Returns to the current device the memory that the library's scratch pool on
+ * it keeps between calls (the rank tables, see the conventions above); later
+ * calls take it from the device again.  Memory of calls still in flight on a
+ * stream is not released.  FSCHED_OK (also when the pool was never created),
+ * or FSCHED_EDEVICE. */
+int fsched_release_cache(void);
+
 #ifdef __cplusplus
 }
 #endif

@@ -34,7 +34,8 @@ METRICS_DTYPE = np.dtype([(f, np.int64) for f in METRIC_FIELDS[:12]] +
                          [("max_extent", np.int32), ("max_active", np.int32)])
 METRICS_BYTES = 104
 EXPORTS = ("fsched_simulate", "fsched_simulate_robust", "fsched_cost_decompose", "fsched_bruteforce_opt",
-           "fsched_strerror", "fsched_abi_version", "fsched_last_hip_error")
+           "fsched_strerror", "fsched_abi_version", "fsched_last_hip_error",
+           "fsched_release_cache")
 
 
 class Params(ctypes.Structure):
@@ -70,12 +71,20 @@ def lib():
         L.fsched_cost_decompose.argtypes = [P, I64, I32, P, P, P, P, P, P, P]
         L.fsched_bruteforce_opt.argtypes = [P, I64, I32, P, P, P, P, P, P]
         for f in (L.fsched_simulate, L.fsched_simulate_robust, L.fsched_cost_decompose, L.fsched_bruteforce_opt,
-                  L.fsched_abi_version, L.fsched_last_hip_error):
+                  L.fsched_abi_version, L.fsched_last_hip_error, L.fsched_release_cache):
             f.restype = ctypes.c_int
         L.fsched_strerror.restype = ctypes.c_char_p
         L.fsched_strerror.argtypes = [ctypes.c_int]
         _lib = L
     return _lib
+
+
+def release_cache() -> None:
+    """Give the memory the library's scratch pool keeps between calls back to the
+    current device (fsched_release_cache)."""
+    rc = lib().fsched_release_cache()
+    if rc:
+        raise FschedError(rc, "fsched_release_cache")
 
 
 def make_params(policy: str = "isjl", B: int = 0, alpha: int = ALPHA_INF, M_kv: int = 0,

@@ -92,8 +92,8 @@ struct Staging {
 // Pool of the rank scratch (2 bytes per job) of the current device, created
 // once: allocations are stream-ordered, and what a call frees stays in the pool
 // (release threshold: never) so that repeated calls allocate nothing new.
-// Null when the device cannot make one.
-hipMemPool_t rank_pool() {
+// Null when the device cannot make one (or, with create false, has none yet).
+hipMemPool_t rank_pool(bool create = true) {
   constexpr int kMaxDev = 64;
   static std::mutex mu;
   static hipMemPool_t pools[kMaxDev] = {};
@@ -104,7 +104,7 @@ hipMemPool_t rank_pool() {
     return nullptr;
   }
   std::lock_guard<std::mutex> g(mu);
-  if (!tried[dev]) {
+  if (!tried[dev] && create) {
     tried[dev] = true;
     hipMemPoolProps props;
     std::memset(&props, 0, sizeof(props));
@@ -291,6 +291,13 @@ const char* fsched_strerror(int code) {
 int fsched_abi_version(void) { return FSCHED_ABI_VERSION; }
 
 int fsched_last_hip_error(void) { return g_last_hip; }
+
+int fsched_release_cache(void) {
+  hipMemPool_t pool = rank_pool(false);
+  if (!pool) return FSCHED_OK;
+  hipError_t e = hipMemPoolTrimTo(pool, 0);
+  return e == hipSuccess ? FSCHED_OK : hip_fail(e);
+}
 
 int fsched_simulate(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
                     const int32_t* arrival, const int32_t* prompt, const int32_t* output,

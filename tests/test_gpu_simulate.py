@@ -390,7 +390,8 @@ def test_fill_sweep_queued_completions(dev, policy, alpha):
 def test_rank_scratch_reuse_across_calls_and_streams(dev):
     """Every policy but FCFS takes its rank table from the library's stream-ordered
     pool: back-to-back calls of different sizes on a side stream (no host sync in
-    between, the earlier tables freed on the stream) each match the oracle."""
+    between, the earlier tables freed on the stream) each match the oracle, and a
+    call after fsched_release_cache gives the same metrics."""
     import torch
     rng = np.random.default_rng(99)
     side = torch.cuda.Stream()
@@ -407,6 +408,11 @@ def test_rank_scratch_reuse_across_calls_and_streams(dev):
             raw, st, fi = fs.simulate(*ts, schedule=True, **kw)
             outs.append((ts, raw, st, fi))
     side.synchronize()
+    fs.release_cache()  # the pool gives its memory back; the next call takes it again
+    a, p, o, kw = jobs[0]
+    again, _, _ = fs.simulate(*[torch.from_numpy(x).to(dev) for x in (a, p, o)], **kw)
+    torch.cuda.synchronize()
+    assert np.array_equal(fs.metrics_view(again), fs.metrics_view(outs[0][1]))
     for (a, p, o, kw), (_, raw, st, fi) in zip(jobs, outs):
         ctx = f"rank scratch reuse {kw}"
         log(ctx)
