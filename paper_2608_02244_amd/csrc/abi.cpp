@@ -135,7 +135,20 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
   const bool isjl = p->policy == FSCHED_ISJL;
   // plan-queue links; with alpha = infinity Phase ONE never plans (no second
   // job is longer than alpha), so the links are not needed
-  const int q_words = (isjl && p->alpha != FSCHED_ALPHA_INF) ? NP / 2 : 0;
+  // (with up to 2 slots per lane, at most 128 VGPRs, 16 waves fit a CU: the
+  // links go to HBM scratch when in LDS they would cap a CU below that)
+  const bool plans = isjl && p->alpha != FSCHED_ALPHA_INF;
+  bool q_hbm = false;
+  if (plans && K <= 2) {
+    const int w_lds = NP + NP / 2 +
+                      std::max((Beff + 1) / 2, 64 * NW);  // words per wave with the links
+    const size_t per_wave = (size_t)((w_lds + 3) & ~3) * 4;
+    int wpb = 4;
+    while (wpb > 1 && per_wave * wpb > 64 * 1024) wpb >>= 1;
+    const size_t waves_per_cu = (160 * 1024) / (per_wave * wpb) * wpb;
+    q_hbm = waves_per_cu < 16;
+  }
+  const int q_words = (plans && !q_hbm) ? NP / 2 : 0;
   // gather buffer (uint16 per worker), also the release scatter buffer (one
   // word per 32 ranks)
   // FCFS gathers nothing, but with 4 or more slots per lane its sweeps pack up to
@@ -163,12 +176,10 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
   a.out_T = out_T;
   a.start = start;
   a.finish = finish;
-  // rank table of the release chunks (not FCFS, whose order is the arrival
-  // order): from the library's pool, else from the device's default pool
-  a.rank_stride = (n + 63) & ~63;
-  a.rank = nullptr;
-  if (p->policy != FSCHED_FCFS) {
-    const size_t bytes = (size_t)n_inst * (size_t)a.rank_stride * 2;
+  // scratch from the library's pool, else from the device's default pool:
+  // the rank table of the release chunks (not FCFS, whose order is the arrival
+  // order) and the HBM plan-queue links
+  auto scratch = [&](size_t bytes) -> void* {
     hipMemPool_t pool = rank_pool();
     void* r = nullptr;
     hipError_t e = pool ? hipMallocFromPoolAsync(&r, bytes, pool, s) : hipErrorNotSupported;
@@ -179,9 +190,27 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
     }
     if (e != hipSuccess) {
       (void)hipGetLastError();
+      return nullptr;
+    }
+    return r;
+  };
+  auto release = [&](void* r) {
+    if (r && hipFreeAsync(r, s) != hipSuccess) (void)hipGetLastError();
+  };
+  a.rank_stride = (n + 63) & ~63;
+  a.rank = nullptr;
+  a.q_stride = NP;
+  a.qlink = nullptr;
+  if (p->policy != FSCHED_FCFS) {
+    a.rank = (uint16_t*)scratch((size_t)n_inst * (size_t)a.rank_stride * 2);
+    if (!a.rank) return FSCHED_ENOMEM;
+  }
+  if (q_hbm) {
+    a.qlink = (uint32_t*)scratch((size_t)n_inst * (size_t)a.q_stride * 4);
+    if (!a.qlink) {
+      release(a.rank);
       return FSCHED_ENOMEM;
     }
-    a.rank = (uint16_t*)r;
   }
 
   hipError_t err = hipSuccess;
@@ -222,7 +251,8 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
     }
     err = e;
   }
-  if (a.rank && hipFreeAsync(a.rank, s) != hipSuccess) (void)hipGetLastError();
+  release(a.rank);
+  release(a.qlink);
   if (err != hipSuccess) return hip_fail(err);
   return FSCHED_OK;
 }

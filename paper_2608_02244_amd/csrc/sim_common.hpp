@@ -46,6 +46,12 @@ struct SimArgs {
   // line is shared by two instances).  Required for every policy but FCFS.
   uint16_t* rank;
   int32_t rank_stride;
+  // Scratch: ISJL plan-queue links of the kernels with up to 2 slots per lane
+  // (rows of q_stride entries; the other kernels keep them in LDS).  Moving
+  // them out of LDS lets 16 waves share a CU.  Null when alpha is infinite
+  // (no plans).
+  uint32_t* qlink;
+  int32_t q_stride;
 };
 
 // Chooses and launches the kernel instantiation for one policy.  `general`

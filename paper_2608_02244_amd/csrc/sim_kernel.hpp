@@ -180,6 +180,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
   uint32_t* W = lds_raw + (size_t)wib * (size_t)a.wave_words;
   int32_t* ARR = (int32_t*)(W + a.off_arr);
   uint16_t* QN = (uint16_t*)(W + a.off_q);
+  // ISJL with up to 2 slots per lane: the plan-queue links live in HBM scratch
+  // when that lets more waves share a CU (agent-scope accesses, so one lane's
+  // link is seen by the others), else in LDS
+  constexpr bool QGLOBAL = POL == POL_ISJL && K <= 2;
+  uint32_t* QG = (QGLOBAL && a.qlink) ? a.qlink + inst * (int64_t)a.q_stride : nullptr;
+  auto qn_set = [&](int r, uint32_t v) {
+    if (QGLOBAL && QG) __hip_atomic_store(QG + r, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else QN[r] = (uint16_t)v;
+  };
+  auto qn_get = [&](int r) -> uint32_t {
+    if (QGLOBAL && QG) return __hip_atomic_load(QG + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return QN[r];
+  };
   uint16_t* STG = (uint16_t*)(W + a.off_stage);
   // Released ranks on their way into the bitmap (not FCFS); shares the gather
   // buffer, which is dead while releases are processed.
@@ -926,8 +939,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
               for (int k = 0; k < K; ++k)
                 if (k == (wsel >> 6)) qt = readlane((int)(ws_q[k] >> 16), wsel & 63);
               if (lane == 0) {
-                if (qt != (int)QNONE) QN[qt] = (uint16_t)r;
-                QN[r] = (uint16_t)QNONE;
+                if (qt != (int)QNONE) qn_set(qt, (uint32_t)r);
+                qn_set(r, QNONE);
               }
 #pragma unroll
               for (int k = 0; k < K; ++k)
@@ -952,18 +965,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
               if (w >= 1 && w < m) {
                 uint32_t r = STG[w];
                 uint32_t h = ws_q[k] & 0xFFFFu, tl = ws_q[k] >> 16;
-                if (tl != QNONE) QN[tl] = (uint16_t)r;
+                if (tl != QNONE) qn_set((int)tl, r);
                 else h = r;
-                QN[r] = (uint16_t)QNONE;
+                qn_set((int)r, QNONE);
                 ws_q[k] = h | (r << 16);
               }
               if (w == 0) {
                 uint32_t r = STG[0];
-                QN[r] = (uint16_t)QNONE;
+                qn_set((int)r, QNONE);
                 ws_q[k] = r | (r << 16);
               }
             }
             wave_lds_sync();
+            // HBM links: every store is done before a plan start reads them
+            if (QGLOBAL && QG) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
             pmax = wave_max(pmax);
             int idle1 = pmax - alpha;
             if (idle1 < 0) idle1 = 0;
@@ -1041,7 +1056,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
               }
               mlen = min(mlen, len);
               emit(pid(wv), t, len);
-              uint32_t nx = QN[h];
+              uint32_t nx = qn_get((int)h);
               ws_q[k] = (nx == QNONE) ? (QNONE | (QNONE << 16)) : (nx | (ws_q[k] & 0xFFFF0000u));
             }
           }

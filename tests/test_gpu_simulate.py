@@ -418,3 +418,32 @@ def test_rank_scratch_reuse_across_calls_and_streams(dev):
         log(ctx)
         ref, rs, rf = oracle.simulate(a, p, o, schedule=True, **kw)
         assert_same(ctx, fs.metrics_view(raw), ref, st.cpu().numpy(), rs, fi.cpu().numpy(), rf)
+
+
+@pytest.mark.parametrize("alpha", [2, 40, 300])
+def test_plan_links_in_hbm(dev, alpha):
+    """ISJL with up to 2 slots per lane and 2,000 jobs: the plan-queue links would
+    cap a CU below 16 waves in LDS, so they go to HBM scratch (also for the
+    predicted-size and prefill variants)."""
+    rng = np.random.default_rng(zlib.crc32(f"qlinks:{alpha}".encode()))
+    for B, M, arr in ((100, 0, 0), (128, 12000, 4000), (70, 6000, -3000)):
+        a, p, o = workload.random_tables(rng, 5, 2000, 60, 200, max_arrival=abs(arr),
+                                         sorted_arrivals=arr > 0)
+        kw = dict(B=B, alpha=alpha, M_kv=M, cost_c=3, cost_tau=1)
+        ctx = f"plan links in HBM alpha={alpha} B={B} M={M} arrivals={arr}"
+        log(ctx)
+        check(dev, ctx, a, p, o, policy="isjl", **kw)
+        log(ctx + " prefill")
+        got, gs, gf = gpu_sim(dev, a, p, o, policy="isjl", prefill=True, **kw)
+        ref, rs, rf = oracle.simulate(a, p, o, policy="isjl", schedule=True,
+                                      flags=oracle.FLAG_PREFILL, **kw)
+        assert_same(ctx + " prefill", got, ref, gs, rs, gf, rf)
+        log(ctx + " robust")
+        u = workload.prediction_upper(o, 0.5, seed=B)
+        import torch
+        ts = [torch.from_numpy(np.ascontiguousarray(x)).to(dev) for x in (a, p, o, u)]
+        raw, st, fi = fs.simulate_robust(*ts, schedule=True, **kw)
+        torch.cuda.synchronize()
+        ref, rs, rf = oracle.simulate_robust(a, p, o, u, schedule=True, **kw)
+        assert_same(ctx + " robust", fs.metrics_view(raw), ref, st.cpu().numpy(), rs,
+                    fi.cpu().numpy(), rf)
