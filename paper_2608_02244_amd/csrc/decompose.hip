@@ -433,17 +433,22 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
     // span terms of every group end of the chunk (the span runs to the next
     // event time; the last event has none)
     if (gend && !last) {
-      const int64_t D = (int64_t)(t_next - t);
+      // times < 2^19 and |S| <= 4,096: the factors below fit 32 bits, so each
+      // product is a 32 x 32 -> 64-bit multiply
+      const int D32 = t_next - t;
+      const int64_t D = D32;
       lD += D;
       if (cnt_p != 0) {
         const int64_t s = cnt_p;
-        const int64_t m0 = (int64_t)(t - gmin) + 1;
-        const int64_t sm = D * m0 + D * (D - 1) / 2;
-        lE += D * (sum_p - s * (int64_t)gmin);
+        const int m0 = t - gmin + 1;
+        const int64_t sm = (int64_t)D32 * m0 + (int64_t)D32 * (D32 - 1) / 2;
+        // sum of (start - earliest start) over the active jobs: < 4,096 x 2^19
+        const int xe = (int)(sum_p - (int64_t)(cnt_p * gmin));
+        lE += (int64_t)D32 * xe;
         lSM += sm;
         lSSM += s * sm;
         const int ext = gmax - gmin;
-        lX += D * ext;
+        lX += (int64_t)D32 * ext;
         lB += D;
         if (ext > alpha) {
           lU += D;
@@ -451,7 +456,7 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
         }
         lXm = max(lXm, ext);
         lAm = max(lAm, cnt_p);
-        lP = max(lP, s * (int64_t)t_next - sum_p);
+        lP = max(lP, (int64_t)(cnt_p * t_next) - sum_p);
         if (Bcap > 0 && cnt_p > Bcap) lcap = true;
         if (M != 0 && cnt_p >= 2 && res_p > M) lkv = true;
       }
