@@ -1795,12 +1795,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
     // (5) next event.  A release is an event only if the job could be admitted
     // before anything else happens: ISJL with an idle worker that has nothing
     // planned in Phase TWO, or an empty machine with no plan; LJF at an empty
-    // machine; FCFS / SJF with a free slot.  Otherwise it is folded into the
+    // machine; SJF with a free slot; FCFS with a free slot and nothing queued
+    // (a queued job left waiting with a slot free is blocked by the KV budget,
+    // which changes only at a completion, and it precedes every later arrival).  Otherwise it is folded into the
     // next event (the queue is only read there).
     int tn = S.min_end;
     bool rel_matters;
     if (POL == POL_ISJL) rel_matters = (mode == 0 && free_empty > 0) || (S.nact == 0 && planned == 0);
     else if (POL == POL_LJF) rel_matters = S.nact == 0;
+    else if (POL == POL_FCFS)  // a queued head blocks every later arrival in FCFS order
+      rel_matters = S.nact < Beff && head == relk;
     else rel_matters = S.nact < Beff;
     if (rel_matters) {
       if (POL == POL_FCFS || !GEN) {
