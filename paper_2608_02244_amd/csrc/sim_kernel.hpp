@@ -1805,7 +1805,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
     else if (POL == POL_LJF) rel_matters = S.nact == 0;
     else if (POL == POL_FCFS)  // a queued head blocks every later arrival in FCFS order
       rel_matters = S.nact < Beff && head == relk;
-    else rel_matters = S.nact < Beff;
+    else if (POL == POL_SJF && !GEN && !PRE && qcount > 0 && S.nact > 0 && S.nact < Beff) {
+      // SJF with a slot free and jobs queued: the queue's head is held back by
+      // the KV budget, which stays fixed until a completion.  An arrival before
+      // then is an event only if it precedes that head in SJF order and fits
+      // beside the running jobs; the first such arrival bounds the span.
+      rel_matters = false;
+      const int hr = pool.first();
+      int r = relk;
+      while (r < n) {
+        if ((r >> 6) != chunk) load_chunk(r >> 6);
+        const int off = r & (WAVE - 1);
+        const bool in = lane >= off && rel_t < tn;
+        const bool m = in && rel_r < hr && S.res + (int64_t)plen(W[rel_r]) <= M;
+        const uint64_t mm = ballot(m);
+        if (mm) {
+          tn = min(tn, readlane(rel_t, __builtin_ctzll(mm)));
+          break;
+        }
+        if (ballot(lane >= off && rel_t >= tn)) break;  // the rest arrive after the span
+        r = (r & ~(WAVE - 1)) + WAVE;
+      }
+    } else rel_matters = S.nact < Beff;
     if (rel_matters) {
       if (POL == POL_FCFS || !GEN) {
         if (relk < n) {
