@@ -1805,11 +1805,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
     else if (POL == POL_LJF) rel_matters = S.nact == 0;
     else if (POL == POL_FCFS)  // a queued head blocks every later arrival in FCFS order
       rel_matters = S.nact < Beff && head == relk;
-    else if (POL == POL_SJF && !GEN && !PRE && qcount > 0 && S.nact > 0 && S.nact < Beff) {
-      // SJF with a slot free and jobs queued: the queue's head is held back by
-      // the KV budget, which stays fixed until a completion.  An arrival before
-      // then is an event only if it precedes that head in SJF order and fits
-      // beside the running jobs; the first such arrival bounds the span.
+    else rel_matters = S.nact < Beff;
+    // ISJL in FILL (with up to 2 slots per lane) and SJF, with a slot free and
+    // jobs queued: the queue's head is held back by the KV budget, which stays
+    // fixed until a completion.  An arrival before then is an event only if it
+    // precedes that head in the policy's order and fits beside the running jobs;
+    // the first such arrival bounds the span.
+    const bool blocked_head =
+        !GEN && !PRE && !ROB && qcount > 0 && S.nact > 0 &&
+        ((POL == POL_SJF && S.nact < Beff) ||
+         (POL == POL_ISJL && K <= 2 && mode == 0 && free_empty > 0 && kv_block));
+    if (blocked_head) {
       rel_matters = false;
       const int hr = pool.first();
       int r = relk;
@@ -1826,7 +1832,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
         if (ballot(lane >= off && rel_t >= tn)) break;  // the rest arrive after the span
         r = (r & ~(WAVE - 1)) + WAVE;
       }
-    } else rel_matters = S.nact < Beff;
+    }
     if (rel_matters) {
       if (POL == POL_FCFS || !GEN) {
         if (relk < n) {
