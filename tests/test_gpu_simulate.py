@@ -449,18 +449,19 @@ def test_plan_links_in_hbm(dev, alpha):
                     fi.cpu().numpy(), rf)
 
 
-@pytest.mark.parametrize("policy", ["fcfs", "sjf"])
-def test_releases_behind_a_blocked_head(dev, policy):
+@pytest.mark.parametrize("policy,alpha", [("fcfs", ALPHA_INF), ("sjf", ALPHA_INF),
+                                          ("isjl", 25), ("isjl", 300), ("isjl", ALPHA_INF)])
+def test_releases_behind_a_blocked_head(dev, policy, alpha):
     """Dense releases while the KV budget holds the queue's head back with slots
-    free: FCFS takes no release as an event while something is queued, SJF only
-    an arrival that precedes the head and fits (in sorted and unsorted release
-    order)."""
-    rng = np.random.default_rng(zlib.crc32(f"blocked-head:{policy}".encode()))
+    free: FCFS takes no release as an event while something is queued, SJF and
+    ISJL in FILL only an arrival that precedes the head and fits (in sorted and
+    unsorted release order)."""
+    rng = np.random.default_rng(zlib.crc32(f"blocked-head:{policy}:{alpha}".encode()))
     for n, B, M, arr in ((1000, 64, 3000, 600), (700, 16, 900, 1400), (1500, 100, 5000, -900),
                          (300, 40, 400, 2000)):
         a, p, o = workload.random_tables(rng, 6, n, 50, 120, max_arrival=abs(arr),
                                          sorted_arrivals=arr > 0)
-        ctx = f"blocked head {policy} n={n} B={B} M={M} arrivals={arr}"
+        ctx = f"blocked head {policy} alpha={alpha} n={n} B={B} M={M} arrivals={arr}"
         log(ctx)
-        check(dev, ctx, a, p, o, policy=policy, B=B, alpha=ALPHA_INF, M_kv=M, cost_c=1,
+        check(dev, ctx, a, p, o, policy=policy, B=B, alpha=alpha, M_kv=M, cost_c=1,
               cost_tau=1)
