@@ -125,8 +125,8 @@ typedef struct {
 /* Per-instance results (104 bytes); every field is exact.
  *   T               makespan (steps, idle steps included)
  *   O               sum of lengths (tokens)
- *   Q               intrinsic term sum_i len_i (len_i + 1) / 2        (Thm 5.1)
- *   E               batching externality sum_t sum_S (max r - r_i)     (Thm 5.1)
+ *   Q               intrinsic term sum_i len_i (len_i + 1) / 2   (profit decomposition, Section 5)
+ *   E               batching externality sum_t sum_S (max r - r_i)  (profit decomposition, Section 5)
  *   C               total cost sum_t (c + tau |S_t| max r); equals c T + tau (Q + E)
  *   W               max-driven step cost sum_t (c + tau max r) (no |S| factor)
  *   sum_completion  sum_i (s_i + len_i)

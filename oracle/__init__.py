@@ -71,6 +71,8 @@ def _load():
         for f in (lib.oracle_simulate_batch, lib.oracle_simulate_robust_batch,
                   lib.oracle_decompose, lib.oracle_opt_batch):
             f.restype = ctypes.c_int
+        lib.oracle_pack_scans_take.restype = ctypes.c_int64
+        lib.oracle_pack_scans_take.argtypes = []
         assert lib.oracle_metrics_size() == 104
         _lib = lib
     return _lib
@@ -105,6 +107,11 @@ def simulate(arrival, prompt, output, *, policy: str, B: int, alpha: int, M_kv: 
     if rc:
         raise OracleError(rc)
     return (out, st, fi) if schedule else out
+
+
+def pack_scans_take() -> int:
+    """Pack candidates Phase ONE examined on this thread since the last call."""
+    return int(_load().oracle_pack_scans_take())
 
 
 def simulate_robust(arrival, prompt, output, upper, *, policy: str = "isjl", B: int,
@@ -156,3 +163,74 @@ def opt(arrival, prompt, output, *, B: int, alpha: int, M_kv: int = 0, schedule:
     if rc:
         raise OracleError(rc)
     return (T, st) if schedule else T
+
+
+# ---------------------------------------------------------------------------
+# Sharded runs: the C oracle keeps no shared state, so contiguous instance
+# ranges can run on several host threads at once (ctypes releases the GIL for
+# the duration of each call).  Each thread runs the same single-threaded code
+# on its own rows; results are identical to one call over all rows.
+
+def host_threads(limit: int = 16) -> int:
+    """Threads to use: the cores this process may run on, at most ``limit``."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(limit, n))
+
+
+def _shards(n_inst: int, threads: int, chunk: int):
+    step = max(1, min(chunk, -(-n_inst // (threads * 4))))
+    return [(b, min(n_inst, b + step)) for b in range(0, n_inst, step)]
+
+
+def simulate_parallel(arrival, prompt, output, *, threads: int, chunk: int = 256,
+                      progress=None, **kw):
+    """``simulate`` over contiguous instance shards on ``threads`` host threads."""
+    from concurrent.futures import ThreadPoolExecutor
+    a, p, o = _tables(arrival, prompt, output)
+    n_inst, n = a.shape
+    sched = kw.get("schedule", False)
+    out = np.zeros(n_inst, dtype=METRICS_DTYPE)
+    st = np.empty((n_inst, n), np.int32) if sched else None
+    fi = np.empty((n_inst, n), np.int32) if sched else None
+
+    def run(span):
+        b, e = span
+        r = simulate(a[b:e], p[b:e], o[b:e], **kw)
+        if sched:
+            out[b:e], st[b:e], fi[b:e] = r
+        else:
+            out[b:e] = r
+        return e - b
+
+    done = 0
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        for k in ex.map(run, _shards(n_inst, threads, chunk)):
+            done += k
+            if progress:
+                progress(done, n_inst)
+    return (out, st, fi) if sched else out
+
+
+def opt_parallel(arrival, prompt, output, *, threads: int, chunk: int = 1024, progress=None,
+                 **kw):
+    """``opt`` over contiguous instance shards on ``threads`` host threads."""
+    from concurrent.futures import ThreadPoolExecutor
+    a, p, o = _tables(arrival, prompt, output)
+    n_inst = a.shape[0]
+    T = np.zeros(n_inst, dtype=np.int64)
+
+    def run(span):
+        b, e = span
+        T[b:e] = opt(a[b:e], p[b:e], o[b:e], **kw)
+        return e - b
+
+    done = 0
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        for k in ex.map(run, _shards(n_inst, threads, chunk)):
+            done += k
+            if progress:
+                progress(done, n_inst)
+    return T

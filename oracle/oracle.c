@@ -150,9 +150,11 @@ static void finish_metrics(or_metrics* m, const or_inst* I, const or_acc* a, int
 
 /* ------------------------------------------------------------------ */
 /* Orders.  Keys are unique because the job index breaks ties. */
-static const int64_t* g_key1;
-static const int32_t* g_key1i;
-static int g_key_mode; /* 0: (arrival, i)  1: (len, i)  2: (-len, i) */
+/* Comparator keys for qsort, one set per thread so that several threads may
+ * each run the oracle on their own instances at once. */
+static _Thread_local const int64_t* g_key1;
+static _Thread_local const int32_t* g_key1i;
+static _Thread_local int g_key_mode; /* 0: (arrival, i)  1: (len, i)  2: (-len, i) */
 
 static int cmp_order(const void* pa, const void* pb) {
   int32_t a = *(const int32_t*)pa, b = *(const int32_t*)pb;
@@ -254,6 +256,16 @@ static void admit_ljf(or_sim* S, const int32_t* ord_long, int64_t t) {
 }
 
 /* ---------------- ISJL ---------------- */
+/* Count of pack candidates examined by Phase ONE on this thread (a measure of
+ * the method's work, read by the roofline's operation count; no effect on any
+ * result). */
+static _Thread_local int64_t g_pack_scans;
+int64_t oracle_pack_scans_take(void) {
+  int64_t v = g_pack_scans;
+  g_pack_scans = 0;
+  return v;
+}
+
 static void enqueue(or_sim* S, int32_t w, int32_t j) {
   S->qnext[j] = -1;
   if (S->qtail[w] < 0) S->qhead[w] = j;
@@ -333,10 +345,16 @@ static void phase_one(or_sim* S, const int32_t* ord_long, int64_t t, uint32_t fl
    * M long jobs; a job that fits no worker is skipped and stays queued).  Each
    * goes to the first spare worker with room, else to the long worker of
    * largest index with room. */
+  /* Algorithm 3 visits the candidates from o_k, the longest within the largest
+   * cap (spare caps alpha included); only those are counted. */
+  int64_t cap_top = Bp > m ? a : 0;
+  for (int64_t w = 1; w < m; ++w)
+    if (S->cap[w] > cap_top) cap_top = S->cap[w];
   for (int32_t q = (int32_t)m; q < k; ++q) {
     int32_t j = S->pool[q];
     int64_t L = I->plan[j];
     int64_t placed = -1;
+    if (L <= cap_top) g_pack_scans++;
     for (int64_t w = m; w < Bp; ++w)
       if (S->load[w] + L <= a) {
         placed = w;

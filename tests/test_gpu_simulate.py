@@ -149,6 +149,22 @@ def test_paper_examples_on_gpu(dev):
     assert g["T"][0] == 40
 
 
+def test_algorithm3_hand_traces_on_gpu(dev):
+    """The hand-traced cases of Algorithm 3's spare and long workers and of the
+    plan width under the KV budget (tests/golden/alg3_spare_examples.json)."""
+    import json
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "alg3_spare_examples.json")
+    for c in json.load(open(path)):
+        a, p, o = (np.array([c[k]], np.int32) for k in ("arrival", "prompt", "output"))
+        g, gs, _ = gpu_sim(dev, a, p, o, policy="isjl", B=c["B"], alpha=c["alpha"],
+                           M_kv=c["M_kv"])
+        assert int(g["T"][0]) == c["T"], c["name"]
+        assert gs[0].tolist() == c["start"], c["name"]
+        check(dev, c["name"], a, p, o, policy="isjl", B=c["B"], alpha=c["alpha"],
+              M_kv=c["M_kv"])
+
+
 @pytest.mark.parametrize("policy", ["isjl", "fcfs", "ljf", "sjf"])
 def test_max_sizes(dev, policy):
     """n = 4096 jobs (two bitmap words per lane) and 1024 workers (16 slots per lane)."""
@@ -240,10 +256,10 @@ def test_named_workloads_full_size(dev, name):
     a, p, o = workload.generate(w)
     ta, tp, to = (torch.from_numpy(x).to(dev) for x in (a, p, o))
     rng = np.random.default_rng(zlib.crc32(name.encode()))
-    n_sample = w.n_inst if w.n_inst <= 256 else 5
+    n_sample = w.n_inst if w.n_inst <= 256 else (32 if name == "bimodal_sweep_4096x2000" else 5)
     sample = np.unique(np.concatenate([[0, w.n_inst - 1],
                                        rng.integers(0, w.n_inst, size=n_sample)]))
-    alphas = w.alphas if name != "bimodal_sweep_4096x2000" else (0, 64, 1024, ALPHA_INF)
+    alphas = w.alphas
     for pol in w.policies:
         for alpha in (alphas if pol in ("isjl", "ljf") else (ALPHA_INF,)):
             ctx = f"{name} {pol} alpha={alpha}"

@@ -21,6 +21,8 @@ from oracle import ALPHA_INF
 from workload import random_tables
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+# smallest T_OPT / T_ISJL (beta = alpha, beta*) on the fixed B = 2 sample below
+WORST_B2_SAMPLE = (Fraction(35, 44), Fraction(29, 37))
 
 
 def z(n):
@@ -397,15 +399,15 @@ def floor_beta_star(alpha):
 
 
 def test_b2_competitive_ratio_bounds():
-    """B = 2 on 400 random instances of at most 6 jobs: LJF's ratio T_OPT/T is at
-    least B/(2B-1) = 2/3 (the LJF theorem, Section 3.1).  ISJL's ratio stays at or
-    above 3/4 with beta = alpha (the remark on beta = alpha, Section 3.2) and at or
-    above the B = 2 theorem's bound at the integer beta* used; those two are the
-    paper's claims, which fail on some 8-job instances (recorded in
-    tests/golden/cr_findings.json) but hold on this sample of smaller ones, so a
-    regression in the oracle's ISJL shows up here."""
+    """B = 2 on 400 random instances of at most 6 jobs.  LJF's ratio T_OPT/T is at
+    least B/(2B-1) = 2/3: the LJF theorem of Section 3.1, which holds in general
+    and is asserted on every instance.  ISJL's ratios are not guarantees: the
+    3/4 of the remark on beta = alpha (Section 3.2) and the B = 2 theorem's bound
+    at beta* both fail on recorded 8-job instances (tests/golden/cr_findings.json).
+    So the smallest ISJL ratios on this fixed sample are pinned as regression
+    values (exact fractions), not checked against those claims."""
     rng = np.random.default_rng(15)
-    worst = Fraction(1)
+    worst_a, worst_b = Fraction(1), Fraction(1)
     for trial in range(400):
         n = int(rng.integers(2, 7))
         alpha = int(rng.integers(1, 9))
@@ -414,11 +416,11 @@ def test_b2_competitive_ratio_bounds():
         T_i = int(sim1(lengths, "isjl", 2, alpha)[0]["T"])
         T_b = int(sim1(lengths, "isjl", 2, alpha, flags=oracle.FLAG_BETA_SQRT17)[0]["T"])
         T_l = int(sim1(lengths, "ljf", 2, alpha)[0]["T"])
-        assert Fraction(T_opt, T_i) >= Fraction(3, 4)
-        assert Fraction(T_opt, T_b) >= theorem1_bound(alpha, floor_beta_star(alpha))
         assert Fraction(T_opt, T_l) >= Fraction(2, 3)
-        worst = min(worst, Fraction(T_opt, T_i))
-    assert worst < 1
+        assert T_opt <= min(T_i, T_b, T_l)
+        worst_a = min(worst_a, Fraction(T_opt, T_i))
+        worst_b = min(worst_b, Fraction(T_opt, T_b))
+    assert (worst_a, worst_b) == WORST_B2_SAMPLE
 
 
 def test_beta_star_floor_values():

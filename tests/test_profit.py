@@ -90,8 +90,14 @@ def test_isjl_extent_within_alpha_and_ordering(table):
     assert t["FCFS"]["avg_extent"] > max(ext)
     assert t["FCFS"]["profit"] < t["LJF"]["profit"]
     # LJF has the largest profit of all rows, as in the paper's table (its E is 0
-    # and c is small); ISJL's makespan against LJF is a documented difference.
+    # and c is small).
     assert max(v["profit"] for v in t.values()) == t["LJF"]["profit"]
+    # ISJL's makespan is pinned against LJF's: on these replications ISJL under
+    # the adopted reading finishes after LJF at every alpha (the paper prints it
+    # ahead); test_pricing_record.py pins the 200-replication means and keeps
+    # the paper's rows as an expected failure.
+    for a in profit.ALPHAS:
+        assert t[f"ISJL(alpha={a})"]["throughput"] < t["LJF"]["throughput"]
 
 
 def test_cost_identity_in_integers():
