@@ -9,7 +9,8 @@ logical step of one instance, so a step contributes sum_i T_i instance-steps.
 
 Prints one JSON line: the metric, the simulate kernel's position against the
 int32 VALU peak (algorithmic lane operations per launch over the measured launch
-time) and the single-core oracle's rate on a sample of the same workload.
+time) and the oracle's rate on this host's cores (all of them, and one) on a
+sample of the same workload.
 """
 from __future__ import annotations
 
@@ -55,20 +56,104 @@ def measured_traffic():
     return int(vals["traffic_bytes_per_launch"])
 
 
-def algorithmic_ops(n_inst: int, n: int, B: int, policy: str, sorted_arrivals: bool) -> float:
-    """Lane operations the event-driven method needs per launch:
-    ordering by a bitonic network (2 per compare-exchange), and per job one
-    admission and one completion, each scanning the B-slot active table once
-    (B compares) plus the table reductions after the completion (B), and one rank
-    lookup (ceil(log2 n) + 1 compares)."""
+COUNTS_FILE = os.path.join(ROOT, "tests", "golden", "roofline_counts.json")
+
+
+def sort_compare_exchanges(n: int) -> int:
+    """Compare-exchanges of a bitonic network over NP = 2^ceil(log2 n) keys
+    (at least 64): NP/2 L (L + 1) / 2 with L = log2 NP."""
     NP = 64
     while NP < n:
         NP *= 2
     L = NP.bit_length() - 1
-    sort_ce = (NP // 2) * L * (L + 1) // 2
+    return (NP // 2) * L * (L + 1) // 2
+
+
+def unit_counts(workload_name: str, policy: str, alpha) -> dict:
+    """The per-instance event and Phase ONE counts measured with the oracle on the
+    workload's first instances (tests/golden/roofline_counts.json)."""
+    key = "inf" if alpha in ("inf", 2**31 - 1) else alpha
+    with open(COUNTS_FILE) as fh:
+        for r in json.load(fh)["runs"]:
+            if (r["workload"], r["policy"], r["alpha"]) == (workload_name, policy, key):
+                return r
+    raise KeyError(f"no unit counts for {workload_name} {policy} alpha={alpha}")
+
+
+def algorithmic_ops(workload_name: str, n_inst: int, n: int, B: int, policy: str, alpha,
+                    sorted_arrivals: bool) -> float:
+    """Int32 lane operations the method needs per launch, from the three work
+    terms of the hot path's measurement model:
+      ordering     2 per compare-exchange of a bitonic network on the n keys
+                   (a min and a max); none for FCFS over arrivals in index order;
+      events       each job starts once and completes once; each of these 2n
+                   events passes once over the active set S: ceil(|S| / 64)
+                   wave operations of 64 lanes (mean sum per instance measured);
+      Phase ONE    each pack candidate Algorithm 3 visits (from o_k on) is placed
+                   first-fit by one ballot per 64 workers: ceil(B / 64) wave
+                   operations (mean count per instance measured).
+    The measured means come from the oracle (tests/golden/make_roofline_counts.py)."""
+    c = unit_counts(workload_name, policy, alpha)
     needs_sort = policy != "fcfs" or not sorted_arrivals
-    per_inst = (2 * sort_ce if needs_sort else 0) + n * (3 * min(B, n) + L + 1)
+    per_inst = (2 * sort_compare_exchanges(n) if needs_sort else 0) \
+        + 64 * c["event_wave_ops_per_instance"] \
+        + 64 * ((min(B, n) + 63) // 64) * c["pack_candidates_per_instance"]
     return float(n_inst) * per_inst
+
+
+def profiled_valu_busy():
+    """Fraction of the launch the SIMDs spent issuing VALU instructions (from the
+    committed counter summary: SQ_INSTS_VALU x 4 cycles per wave64 instruction
+    over 1,024 SIMDs at 2.4 GHz, divided by the traced launch time), or None once
+    the kernel sources differ from the ones the counters were taken with."""
+    try:
+        text = open(TRAFFIC_SUMMARY).read()
+    except OSError:
+        return None
+    vals = dict(line.split(": ", 1) for line in text.splitlines() if ": " in line)
+    if vals.get("kernel_sources_sha256", "").strip() != kernel_sources_sha256():
+        return None
+    v = vals.get("valu_busy_fraction")
+    return None if v is None else float(v)
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def oracle_baseline(np, a, p, o, m_gpu, fields, kw, seconds: float) -> dict:
+    """The single-threaded C oracle timed on this host's cores: on one core over
+    a leading sample, and on every core this process may use (one contiguous
+    shard of instances per thread, at most 16) over a larger leading sample;
+    both checked against the GPU's metrics."""
+    import oracle
+    n_inst = a.shape[0]
+    c0 = time.perf_counter()
+    oracle.simulate(a[:1], p[:1], o[:1], **kw)
+    one = max(time.perf_counter() - c0, 1e-4)
+    k1 = int(max(1, min(n_inst, seconds / 2 / one)))
+    c0 = time.perf_counter()
+    ref1 = oracle.simulate(a[:k1], p[:k1], o[:k1], **kw)
+    s1 = time.perf_counter() - c0
+    threads = oracle.host_threads()
+    kn = int(max(k1, min(n_inst, k1 * threads)))
+    c0 = time.perf_counter()
+    refn = oracle.simulate_parallel(a[:kn], p[:kn], o[:kn], threads=threads, chunk=8, **kw)
+    sn = time.perf_counter() - c0
+    parity = all(np.array_equal(refn[f], m_gpu[f][:kn]) for f in fields) and \
+        all(np.array_equal(ref1[f], m_gpu[f][:k1]) for f in fields)
+    return {"value": float(refn["T"].sum()) / sn, "unit": UNIT, "cores": threads,
+            "kind": "oracle",
+            "sample": f"first {kn} instances on {threads} threads ({sn:.1f} s); one core: "
+                      f"first {k1} instances ({s1:.1f} s)",
+            "value_1core": float(ref1["T"].sum()) / s1, "nproc": os.cpu_count(),
+            "cpu_model": cpu_model(), "parity_on_sample": parity}
 
 
 def main() -> int:
@@ -174,12 +259,13 @@ def main() -> int:
     ms_per_step = wall / args.steps * 1e3
     value = inst_steps * args.steps / wall
 
-    ops = algorithmic_ops(w.n_inst, w.n_jobs, w.B, policy, sorted_arrivals)
+    ops = algorithmic_ops(w.name, w.n_inst, w.n_jobs, w.B, policy, alpha, sorted_arrivals)
     achieved = ops / avg_launch_s
     roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_ALU / 1e12,
                 "unit": "Tops/s (int32 lane operations)", "frac": achieved / PEAK_ALU,
                 "traffic": measured_traffic(), "kernel": f"simulate_kernel<ISJL> ({w.n_inst} waves)",
-                "avg_launch_ms": avg_launch_s * 1e3, "ops_per_launch": ops}
+                "avg_launch_ms": avg_launch_s * 1e3, "ops_per_launch": ops,
+                "valu_busy_profiled": profiled_valu_busy()}
 
     out = {"metric": METRIC, "value": value, "unit": UNIT, "n_gpus": 1, "steps": args.steps,
            "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
@@ -194,23 +280,10 @@ def main() -> int:
         out["alpha_sweep"] = alpha_sweep(torch, np, workload, fs, stream)
 
     if not args.no_cpu_baseline:
-        import oracle
         kw_o = dict(policy=policy, B=w.B, alpha=alpha, M_kv=w.M_kv, cost_c=w.cost_c,
                     cost_tau=w.cost_tau)
-        c0 = time.perf_counter()
-        oracle.simulate(a[:1], p[:1], o[:1], **kw_o)
-        one = max(time.perf_counter() - c0, 1e-4)
-        k = int(max(1, min(w.n_inst, args.cpu_seconds / one)))
-        c0 = time.perf_counter()
-        ref = oracle.simulate(a[:k], p[:k], o[:k], **kw_o)
-        cpu_s = time.perf_counter() - c0
-        parity = all(np.array_equal(ref[f], m[f][:k]) for f in fs.METRIC_FIELDS)
-        out["cpu_baseline"] = {"value": float(ref["T"].sum()) / cpu_s, "unit": UNIT, "cores": 1,
-                               "kind": "oracle",
-                               "sample": f"first {k} of {w.n_inst} instances of {w.name} "
-                                         f"(ISJL alpha={alpha}), single-threaded C oracle, "
-                                         f"{cpu_s:.1f} s",
-                               "parity_on_sample": parity}
+        out["cpu_baseline"] = oracle_baseline(np, a, p, o, m, fs.METRIC_FIELDS, kw_o,
+                                              args.cpu_seconds)
     print(json.dumps(out), flush=True)
     return 0
 
@@ -223,9 +296,9 @@ def alpha_sweep(torch, np, workload, fs, stream, reps: int = 5, alphas=None) -> 
     a, p, o = workload.generate(w)
     sorted_arrivals = bool((np.diff(a, axis=1) >= 0).all())
     ta, tp, to = (torch.from_numpy(x).to("cuda:0") for x in (a, p, o))
-    ops = algorithmic_ops(w.n_inst, w.n_jobs, w.B, "isjl", sorted_arrivals)
     rows = []
     for al in (w.alphas if alphas is None else alphas):
+        ops = algorithmic_ops(w.name, w.n_inst, w.n_jobs, w.B, "isjl", al, sorted_arrivals)
         kw = dict(policy="isjl", B=w.B, alpha=al, M_kv=w.M_kv, cost_c=w.cost_c,
                   cost_tau=w.cost_tau)
         raw, _, _ = fs.simulate(ta, tp, to, **kw)
@@ -242,9 +315,10 @@ def alpha_sweep(torch, np, workload, fs, stream, reps: int = 5, alphas=None) -> 
             ms.append(e0.elapsed_time(e1))
         t = sorted(ms)[len(ms) // 2] / 1e3
         rows.append({"alpha": "inf" if al == workload.ALPHA_INF else al, "ms": t * 1e3,
-                     "instance_steps_per_s": steps / t, "frac": ops / t / PEAK_ALU})
+                     "instance_steps_per_s": steps / t, "ops_per_launch": ops,
+                     "frac": ops / t / PEAK_ALU})
     return {"workload": w.name, "policy": "isjl", "B": w.B, "M_kv": w.M_kv,
-            "ops_per_launch": ops, "bound": "alu", "results": rows}
+            "bound": "alu", "results": rows}
 
 
 def time_host(torch, np, workload, fs, args) -> int:
