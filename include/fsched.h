@@ -76,7 +76,9 @@ enum {
   FSCHED_EDEVICE = -4,   /* a HIP call failed (see fsched_last_hip_error)     */
   FSCHED_ETOOLARGE = -5, /* beyond a kernel limit                            */
   FSCHED_ENOTIMPL = -6,
-  FSCHED_EINTERNAL = -7  /* an instance found no next event, or its exact search hit its cap */
+  FSCHED_EINTERNAL = -7, /* an instance found no next event, or its exact search hit its cap */
+  FSCHED_ESCRATCH = -8   /* fsched_simulate_noalloc: the call needs more scratch than
+                            FSCHED_NOALLOC_SCRATCH_BYTES                         */
 };
 
 /* Per-instance markers written into fsched_metrics.T in device mode. */
@@ -235,6 +237,35 @@ int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs
 int fsched_bruteforce_opt(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
                           const int32_t* arrival, const int32_t* prompt, const int32_t* output,
                           int64_t* T_opt, int32_t* start_opt, void* stream);
+
+/* fsched_simulate_noalloc — fsched_simulate for callers that cannot allocate
+ * device memory during the call: code being captured into a HIP graph, tight
+ * serving loops, harnesses that forbid hipMalloc.  It allocates nothing: no
+ * hipMalloc / hipFree / pool allocation and no host staging.  Its scratch (the
+ * rank table of 2 bytes per job, rows rounded up to 64 jobs, for every policy
+ * but FCFS; for ISJL with at most 128 workers and a finite alpha, when the
+ * plan-queue links do not fit LDS, 4 bytes per job rounded up to a power of two
+ * (at least 64)) is a fixed buffer of FSCHED_NOALLOC_SCRATCH_BYTES per device,
+ * part of the library's image and held by each device the library runs on
+ * until the process ends; its device address is looked up once per device, on
+ * that device's first call.
+ *   - p->flags must include FSCHED_F_DEVICE_PTRS (EINVAL otherwise); every
+ *     array is a device pointer on the current device, and outputs as in
+ *     fsched_simulate.  FSCHED_F_SYNC synchronises the stream before return.
+ *   - A call whose scratch would exceed FSCHED_NOALLOC_SCRATCH_BYTES returns
+ *     FSCHED_ESCRATCH before enqueuing anything (e.g. at 2,000 jobs per
+ *     instance and B = 512: 16,384 instances fit 64 MiB).
+ *   - Every call on one device shares that device's buffer: calls that overlap
+ *     in time on one device (on different streams, or from several threads)
+ *     race and give undefined results.  Calls in order on one stream are safe.
+ *     No part of the buffer needs to start cleared (each instance writes its
+ *     rows before it reads them), so the last call's contents do no harm.
+ * Arguments, results and the other errors as fsched_simulate. */
+#define FSCHED_NOALLOC_SCRATCH_BYTES (64u << 20)
+int fsched_simulate_noalloc(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
+                            const int32_t* arrival, const int32_t* prompt,
+                            const int32_t* output, fsched_metrics* out, int32_t* start,
+                            int32_t* finish, void* stream);
 
 /* Text for a return code (static storage). */
 const char* fsched_strerror(int code);

@@ -26,6 +26,8 @@ POLICIES = {"fcfs": 0, "ljf": 1, "isjl": 2, "sjf": 3}
 F_DEVICE_PTRS, F_SYNC, F_BETA_SQRT17, F_RESUME_FILL, F_PREFILL = 1, 4, 8, 16, 32
 
 OK, EINVAL, ERANGE, ENOMEM, EDEVICE, ETOOLARGE, ENOTIMPL, EINTERNAL = 0, -1, -2, -3, -4, -5, -6, -7
+ESCRATCH = -8
+NOALLOC_SCRATCH_BYTES = 64 << 20  # FSCHED_NOALLOC_SCRATCH_BYTES
 T_INVALID, T_RANGE, T_TOOLARGE, T_INTERNAL = -1, -2, -5, -7
 
 METRIC_FIELDS = ("T", "O", "Q", "E", "C", "W", "sum_completion", "sum_latency", "sum_extent",
@@ -35,7 +37,7 @@ METRICS_DTYPE = np.dtype([(f, np.int64) for f in METRIC_FIELDS[:12]] +
 METRICS_BYTES = 104
 EXPORTS = ("fsched_simulate", "fsched_simulate_robust", "fsched_cost_decompose", "fsched_bruteforce_opt",
            "fsched_strerror", "fsched_abi_version", "fsched_last_hip_error",
-           "fsched_release_cache")
+           "fsched_release_cache", "fsched_simulate_noalloc")
 
 
 class Params(ctypes.Structure):
@@ -67,10 +69,11 @@ def lib():
         L = ctypes.CDLL(LIB_PATH)
         P, I64, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
         L.fsched_simulate.argtypes = [P, I64, I32, P, P, P, P, P, P, P]
+        L.fsched_simulate_noalloc.argtypes = [P, I64, I32, P, P, P, P, P, P, P]
         L.fsched_simulate_robust.argtypes = [P, I64, I32, P, P, P, P, P, P, P, P]
         L.fsched_cost_decompose.argtypes = [P, I64, I32, P, P, P, P, P, P, P]
         L.fsched_bruteforce_opt.argtypes = [P, I64, I32, P, P, P, P, P, P]
-        for f in (L.fsched_simulate, L.fsched_simulate_robust, L.fsched_cost_decompose, L.fsched_bruteforce_opt,
+        for f in (L.fsched_simulate, L.fsched_simulate_noalloc, L.fsched_simulate_robust, L.fsched_cost_decompose, L.fsched_bruteforce_opt,
                   L.fsched_abi_version, L.fsched_last_hip_error, L.fsched_release_cache):
             f.restype = ctypes.c_int
         L.fsched_strerror.restype = ctypes.c_char_p
@@ -150,6 +153,37 @@ def simulate(arrival, prompt, output, *, policy: str, B: int, alpha: int, M_kv: 
     p = make_params(policy, B, alpha, M_kv, cost_c, cost_tau, beta_sqrt17,
                     device=_is_torch(arrival), resume_fill=resume_fill, prefill=prefill)
     return _simulate("fsched_simulate", p, (arrival, prompt, output), schedule, stream)
+
+
+def simulate_noalloc(arrival, prompt, output, out, *, policy: str, B: int, alpha: int,
+                     M_kv: int = 0, cost_c: int = 0, cost_tau: int = 1,
+                     beta_sqrt17: bool = False, resume_fill: bool = False,
+                     prefill: bool = False, start=None, finish=None, stream=None):
+    """fsched_simulate_noalloc: ``simulate`` on torch device tensors into outputs
+    the caller allocated beforehand (``out`` [n_inst, 13] int64; ``start`` /
+    ``finish`` [n_inst, n_jobs] int32 or None); the library allocates nothing.
+    Enqueued on ``stream`` (default: the current torch stream)."""
+    import torch
+    ts = _torch_tables(arrival, prompt, output)
+    n_inst, n = ts[0].shape
+    for name, x, shape, dt in (("out", out, (n_inst, 13), torch.int64),
+                               ("start", start, (n_inst, n), torch.int32),
+                               ("finish", finish, (n_inst, n), torch.int32)):
+        if x is None and name != "out":
+            continue
+        if x is None or tuple(x.shape) != shape or x.dtype != dt or not x.is_contiguous() \
+                or not x.is_cuda:
+            raise ValueError(f"{name} must be a contiguous {dt} GPU tensor of shape {shape}")
+    p = make_params(policy, B, alpha, M_kv, cost_c, cost_tau, beta_sqrt17, device=True,
+                    resume_fill=resume_fill, prefill=prefill)
+    rc = lib().fsched_simulate_noalloc(ctypes.byref(p), n_inst, n, *[x.data_ptr() for x in ts],
+                                       out.data_ptr(),
+                                       start.data_ptr() if start is not None else None,
+                                       finish.data_ptr() if finish is not None else None,
+                                       _stream_handle(torch, stream))
+    if rc:
+        raise FschedError(rc, "fsched_simulate_noalloc")
+    return out, start, finish
 
 
 def simulate_robust(arrival, prompt, output, upper, *, B: int, alpha: int, M_kv: int = 0,

@@ -11,6 +11,7 @@
 #include "sim_common.hpp"
 #include "dec_common.hpp"
 #include "opt_common.hpp"
+#include "abi_internal.hpp"
 
 namespace {
 
@@ -122,10 +123,17 @@ hipMemPool_t rank_pool(bool create = true) {
   return pools[dev];
 }
 
-int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int32_t* arrival,
-                    const int32_t* prompt, const int32_t* output, fsched_metrics* out,
-                    int64_t* out_T, int32_t* start, int32_t* finish, hipStream_t s,
-                    const int32_t* upper = nullptr) {
+size_t round256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+// Launch shape and scratch layout of one simulate call.
+struct SimLayout {
+  int Beff, K, NW, NP, q_words, stage_words;
+  bool q_hbm;
+  int32_t rank_stride;
+  size_t rank_bytes, qlink_bytes;  // device scratch, each rounded up to 256 bytes
+};
+
+int simulate_layout(const fsched_params* p, int64_t n_inst, int32_t n, SimLayout* L) {
   const int Beff = (p->B == 0 || p->B > n) ? n : p->B;
   if (n > fs::MAX_JOBS || Beff > fs::MAX_WORKERS) return FSCHED_ETOOLARGE;
   int K = 1;
@@ -148,13 +156,42 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
     const size_t waves_per_cu = (160 * 1024) / (per_wave * wpb) * wpb;
     q_hbm = waves_per_cu < 16;
   }
-  const int q_words = (plans && !q_hbm) ? NP / 2 : 0;
+  L->Beff = Beff;
+  L->K = K;
+  L->NW = NW;
+  L->NP = NP;
+  L->q_hbm = q_hbm;
+  L->q_words = (plans && !q_hbm) ? NP / 2 : 0;
   // gather buffer (uint16 per worker), also the release scatter buffer (one
   // word per 32 ranks)
   // FCFS gathers nothing, but with 4 or more slots per lane its sweeps pack up to
   // 64 active slots through this buffer too
-  const int stage_words =
+  L->stage_words =
       p->policy != FSCHED_FCFS ? std::max((Beff + 1) / 2, 64 * NW) : (K >= 4 ? 64 : 0);
+  L->rank_stride = (n + 63) & ~63;
+  // the rank table of the release chunks (not FCFS, whose order is the arrival
+  // order) and the HBM plan-queue links
+  L->rank_bytes =
+      p->policy != FSCHED_FCFS ? round256((size_t)n_inst * (size_t)L->rank_stride * 2) : 0;
+  L->qlink_bytes = q_hbm ? round256((size_t)n_inst * (size_t)NP * 4) : 0;
+  return FSCHED_OK;
+}
+
+// Enqueue the simulate kernels.  Scratch comes from `ext` (ext_bytes long, at
+// least the layout's rank_bytes + qlink_bytes, 256-byte aligned) when given,
+// else from the library's pool.
+int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int32_t* arrival,
+                    const int32_t* prompt, const int32_t* output, fsched_metrics* out,
+                    int64_t* out_T, int32_t* start, int32_t* finish, hipStream_t s,
+                    const int32_t* upper = nullptr, void* ext = nullptr,
+                    size_t ext_bytes = 0) {
+  SimLayout Lay;
+  int lrc = simulate_layout(p, n_inst, n, &Lay);
+  if (lrc) return lrc;
+  const int Beff = Lay.Beff, K = Lay.K, NW = Lay.NW, NP = Lay.NP;
+  const bool q_hbm = Lay.q_hbm;
+  const int q_words = Lay.q_words, stage_words = Lay.stage_words;
+  if (ext && ext_bytes < Lay.rank_bytes + Lay.qlink_bytes) return FSCHED_ESCRATCH;
 
   fs::SimArgs a;
   std::memset(&a, 0, sizeof(a));
@@ -176,10 +213,15 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
   a.out_T = out_T;
   a.start = start;
   a.finish = finish;
-  // scratch from the library's pool, else from the device's default pool:
-  // the rank table of the release chunks (not FCFS, whose order is the arrival
-  // order) and the HBM plan-queue links
+  // scratch from the caller's buffer, else from the library's pool, else from
+  // the device's default pool
+  char* ext_next = (char*)ext;
   auto scratch = [&](size_t bytes) -> void* {
+    if (ext) {
+      void* r = ext_next;
+      ext_next += round256(bytes);
+      return r;
+    }
     hipMemPool_t pool = rank_pool();
     void* r = nullptr;
     hipError_t e = pool ? hipMallocFromPoolAsync(&r, bytes, pool, s) : hipErrorNotSupported;
@@ -195,9 +237,9 @@ int launch_simulate(const fsched_params* p, int64_t n_inst, int32_t n, const int
     return r;
   };
   auto release = [&](void* r) {
-    if (r && hipFreeAsync(r, s) != hipSuccess) (void)hipGetLastError();
+    if (!ext && r && hipFreeAsync(r, s) != hipSuccess) (void)hipGetLastError();
   };
-  a.rank_stride = (n + 63) & ~63;
+  a.rank_stride = Lay.rank_stride;
   a.rank = nullptr;
   a.q_stride = NP;
   a.qlink = nullptr;
@@ -302,6 +344,42 @@ int simulate_entry(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
 
 }  // namespace
 
+namespace fs {
+
+int simulate_scratch_need(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
+                          size_t* bytes) {
+  SimLayout L;
+  int rc = simulate_layout(p, n_inst, n_jobs, &L);
+  if (rc) return rc;
+  *bytes = L.rank_bytes + L.qlink_bytes;
+  return FSCHED_OK;
+}
+
+int simulate_with_scratch(const fsched_params* p, int64_t n_inst, int32_t n_jobs,
+                          const int32_t* arrival, const int32_t* prompt, const int32_t* output,
+                          fsched_metrics* out, int32_t* start, int32_t* finish,
+                          hipStream_t stream, void* scratch, size_t scratch_bytes) {
+  int rc = launch_simulate(p, n_inst, n_jobs, arrival, prompt, output, out, nullptr, start,
+                           finish, stream, nullptr, scratch, scratch_bytes);
+  if (rc) return rc;
+  if (p->flags & FSCHED_F_SYNC) {
+    hipError_t e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  return FSCHED_OK;
+}
+
+int check_simulate_args(const fsched_params* p, int64_t n_inst, int32_t n_jobs) {
+  int rc = check_params(p, true);
+  if (rc) return rc;
+  if (n_inst < 0 || n_jobs < 1) return FSCHED_EINVAL;
+  return FSCHED_OK;
+}
+
+int record_hip_error(hipError_t e) { return hip_fail(e); }
+
+}  // namespace fs
+
 extern "C" {
 
 const char* fsched_strerror(int code) {
@@ -314,6 +392,8 @@ const char* fsched_strerror(int code) {
     case FSCHED_ETOOLARGE: return "instance beyond a kernel limit";
     case FSCHED_ENOTIMPL: return "not implemented";
     case FSCHED_EINTERNAL: return "internal error: no next event";
+    case FSCHED_ESCRATCH:
+      return "the call needs more scratch than fsched_simulate_noalloc's fixed buffer holds";
     default: return "unknown error code";
   }
 }

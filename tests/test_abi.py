@@ -31,7 +31,7 @@ def test_library_exports_every_declared_function():
 def test_abi_version_and_strerror():
     L = fs.lib()
     assert L.fsched_abi_version() == 1
-    for code in (0, -1, -2, -3, -4, -5, -6, -7):
+    for code in (0, -1, -2, -3, -4, -5, -6, -7, -8):
         assert L.fsched_strerror(code)
     assert L.fsched_strerror(12345) == b"unknown error code"
 
@@ -85,3 +85,25 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(fs, "_lib", None)
     with pytest.raises(RuntimeError, match="not built"):
         fs.lib()
+
+
+def call_noalloc(p, n_inst=1, n_jobs=4, ptr=DUMMY):
+    return fs.lib().fsched_simulate_noalloc(ctypes.byref(p) if p is not None else None, n_inst,
+                                            n_jobs, ptr, ptr, ptr, ptr, None, None, None)
+
+
+def test_noalloc_argument_errors_before_device_work():
+    """The no-allocation call refuses host mode (it would have to stage), checks
+    arguments like fsched_simulate, and refuses a shape whose scratch exceeds its
+    fixed buffer with FSCHED_ESCRATCH, all before touching the device."""
+    assert call_noalloc(fs.make_params("isjl", 2, 1, device=False)) == fs.EINVAL
+    assert call_noalloc(None) == fs.EINVAL
+    p = fs.make_params("isjl", 512, 128, device=True)
+    assert call_noalloc(p, n_jobs=0) == fs.EINVAL
+    assert call_noalloc(p, n_inst=0) == fs.OK
+    assert call_noalloc(p, ptr=None) == fs.EINVAL
+    assert call_noalloc(p, n_jobs=4097) == fs.ETOOLARGE
+    # 65,536 x 2,000 jobs: a 256 MiB rank table against the 64 MiB buffer
+    assert call_noalloc(p, n_inst=65536, n_jobs=2000) == fs.ESCRATCH
+    assert call_noalloc(fs.make_params("fcfs", 512, 128, device=True), n_inst=65536,
+                        n_jobs=2000, ptr=None) == fs.EINVAL
