@@ -1572,8 +1572,33 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
           quiet += __builtin_popcountll(ballot(ws_end[k] != IDLE && ws_end[k] <= r_next));
       }
     }
+    // ISJL in FILL (or waiting on worker 1's timer) with A_max(t) > alpha: no
+    // planned start, no Phase TWO admission and no epoch can come before the
+    // first completion after which A_max <= alpha (A_max only grows between
+    // completions, and every start needs it within alpha).  The only decision
+    // meanwhile is Phase TWO's switch to DRAIN, at the first event with an idle
+    // worker that has nothing planned and a queued job; both only appear over
+    // the span, so it is settled from their first times after the sweep.  Taken
+    // when at least two completions come before the last of the oldest active
+    // jobs ends (A_max stays above alpha until then); compiled into the kernels
+    // with up to 2 slots per lane (on the wider ones it did not fire on the
+    // measured workloads and only added code).
+    bool amax_sweep = false;
+    if (POL == POL_ISJL && K <= 2 && !PRE && !FILL && S.nact > 0 && t - S.min_s > alpha &&
+        !(mode == 1 && !w0_timer) && quiet < 3) {
+      int oe = -1;
+#pragma unroll
+      for (int k = 0; k < K; ++k)
+        if (ws_start[k] == S.min_s) oe = max(oe, ws_end[k]);
+      oe = wave_max(oe);
+      int before = 0;
+#pragma unroll
+      for (int k = 0; k < K; ++k) before += __builtin_popcountll(ballot(ws_end[k] < oe));
+      amax_sweep = before >= 2;
+    }
     bool sweep = !PRE &&
-                 (POL == POL_LJF || (POL == POL_ISJL && mode == 1 && !w0_timer) || quiet >= 3) &&
+                 (POL == POL_LJF || (POL == POL_ISJL && mode == 1 && !w0_timer) || quiet >= 3 ||
+                  amax_sweep) &&
                  S.nact > 0;
     if (sweep) {
       const int N = S.nact;
@@ -1663,7 +1688,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
         // the machine is empty or A_max <= alpha (A_max right after the
         // completions at e is e - t + the largest progress still active).
         stop = quiet >= 3 ? quiet - 1 : N - 1;
-        if (POL == POL_ISJL && (planned > 0 || (a.resume && mode == 1))) {
+        if (POL == POL_ISJL && (planned > 0 || (a.resume && mode == 1) || amax_sweep)) {
           int cg_max = xs_max, lfound = IDLE;
 #pragma unroll
           for (int k = KS - 1; k >= 0; --k) {
@@ -1758,6 +1783,39 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
       acc_busy += span;
       acc_unfair += wave_sum(lU);
       acc_peak = max(acc_peak, wave_max64(lP));
+      if (POL == POL_ISJL && amax_sweep && mode == 0) {
+        // Phase TWO switches to DRAIN at the first event before tau_end with an
+        // idle worker that has nothing planned (from its first completion, or
+        // now) and a queued job (now, or from the next release)
+        int tn_free = IDLE;
+        if (planned == 0 && S.nact < Beff) {
+          tn_free = t;
+        } else {
+          int fe = IDLE;
+          bool idle_empty = false;
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            const bool empty_q = (ws_q[k] & 0xFFFFu) == QNONE;
+            if (valid[k] && empty_q) {
+              if (ws_end[k] == IDLE) idle_empty = true;
+              else fe = min(fe, ws_end[k]);
+            }
+          }
+          tn_free = ballot(idle_empty) ? t : wave_min(fe);
+        }
+        int tn_queued = IDLE;
+        if (qcount > 0) {
+          tn_queued = t;
+        } else if (POL == POL_FCFS || !GEN) {
+          if (relk < n) {
+            if ((relk >> 6) != chunk) load_chunk(relk >> 6);
+            tn_queued = readlane(rel_t, relk & (WAVE - 1));
+          }
+        } else {
+          tn_queued = next_rel;
+        }
+        if (max(tn_free, tn_queued) < tau_end) mode = 1;
+      }
       // retire every job that completed by tau_end
       int rc = 0, rl = 0, me = IDLE;
 #pragma unroll
