@@ -171,7 +171,7 @@ def main() -> int:
                     help="skip the per-alpha roofline lines of the fairness-budget sweep workload")
     ap.add_argument("--mode", default="simulate",
                     choices=["simulate", "copy", "decompose", "opt", "host", "profit",
-                             "gamma", "robust", "efficiency", "prefill", "sweep"],
+                             "gamma", "robust", "efficiency", "prefill", "sweep", "configs"],
                     help="simulate: the benchmark line; copy: a plain device copy of known size "
                          "(calibrates the HBM byte counters); decompose / opt: time the other "
                          "two library calls (for profiles); host: host-buffer calls, "
@@ -181,7 +181,10 @@ def main() -> int:
                          "instances); efficiency: throughput and AEL of every policy on the "
                          "LMSYS-shaped workload; prefill: the prefill-at-admission variant "
                          "of every policy on pareto_65536x2000; sweep: the fairness-budget "
-                         "sweep alone (--alpha to pick one budget, for counter runs)")
+                         "sweep alone (--alpha to pick one budget, for counter runs); "
+                         "configs: every named workload under each of its policies and "
+                         "budgets, GPU rate, roofline fraction and the oracle on one and on "
+                         "every host core (the results table of the baseline notes)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the instances are "
@@ -212,6 +215,8 @@ def main() -> int:
         return time_efficiency(np, workload)
     if args.mode == "prefill":
         return time_prefill(torch, np, workload, fs, args)
+    if args.mode == "configs":
+        return time_configs(torch, np, workload, fs, args)
     if args.mode == "sweep":
         alphas = None
         if args.alpha is not None:
@@ -285,6 +290,117 @@ def main() -> int:
         out["cpu_baseline"] = oracle_baseline(np, a, p, o, m, fs.METRIC_FIELDS, kw_o,
                                               args.cpu_seconds)
     print(json.dumps(out), flush=True)
+    return 0
+
+
+def _median_launch_ms(torch, fn, reps: int = 5) -> float:
+    stream = torch.cuda.current_stream()
+    fn()
+    torch.cuda.synchronize()
+    ms = []
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms.append(e0.elapsed_time(e1))
+    return sorted(ms)[len(ms) // 2]
+
+
+def time_configs(torch, np, workload, fs, args) -> int:
+    """Every named workload of the benchmark target under each of its policies
+    and fairness budgets: the sum of makespans, GPU instance-steps/s (HIP events,
+    median of 5 launches over the whole table in HBM), the fraction of the ALU
+    roofline under the three-term operation count, and the oracle's rate on one
+    core and on every host core (leading samples, checked against the GPU)."""
+    import oracle
+    INF = workload.ALPHA_INF
+    plan = [("uniform_256x64", [("fcfs", INF), ("ljf", 8), ("isjl", 8)]),
+            ("lognormal_4096x1000", [("fcfs", INF), ("ljf", 64), ("isjl", 64)]),
+            ("bimodal_sweep_4096x2000", [("isjl", al) for al in (0, 16, 64, 256, 1024, INF)]
+             + [("fcfs", INF), ("ljf", 64)]),
+            ("pareto_65536x2000", [("isjl", 128)])]
+    rows = []
+    threads = oracle.host_threads()
+    secs = max(0.5, args.cpu_seconds / 8)
+    for name, runs in plan:
+        w = workload.WORKLOADS[name]
+        a, p, o = workload.generate(w)
+        sorted_arrivals = bool((np.diff(a, axis=1) >= 0).all())
+        ta, tp, to = (torch.from_numpy(x).to("cuda:0") for x in (a, p, o))
+        for pol, al in runs:
+            kw = dict(policy=pol, B=w.B, alpha=al, M_kv=w.M_kv, cost_c=w.cost_c,
+                      cost_tau=w.cost_tau)
+            raw, _, _ = fs.simulate(ta, tp, to, **kw)
+            torch.cuda.synchronize()
+            m = fs.metrics_view(raw).copy()
+            if (m["T"] < 0).any():
+                raise RuntimeError(f"{name} {pol}: error marker")
+            steps = int(m["T"].sum())
+            ms = _median_launch_ms(torch, lambda: fs.simulate(ta, tp, to, **kw))
+            try:
+                ops = algorithmic_ops(name, w.n_inst, w.n_jobs, w.B, pol, al, sorted_arrivals)
+                frac = ops / (ms / 1e3) / PEAK_ALU
+            except KeyError:
+                ops = frac = None
+            cpu = oracle_baseline(np, a, p, o, m, fs.METRIC_FIELDS, kw, secs)
+            row = {"workload": name, "policy": pol, "alpha": "inf" if al == INF else al,
+                   "sum_T": steps, "gpu_ms": ms, "gpu_instance_steps_per_s": steps / (ms / 1e3),
+                   "alu_frac": frac, "ops_per_launch": ops,
+                   "oracle_1core": cpu["value_1core"], "oracle_all_cores": cpu["value"],
+                   "oracle_threads": threads, "parity_on_samples": cpu["parity_on_sample"]}
+            print(json.dumps(row), file=sys.stderr, flush=True)
+            rows.append(row)
+        del ta, tp, to
+        torch.cuda.empty_cache()
+    # the tiny workload: ISJL and the exact optimum for every (alpha, KV budget)
+    w = workload.WORKLOADS["tiny_opt_1048576x8"]
+    a, p, o = workload.generate(w)
+    ta, tp, to = (torch.from_numpy(x).to("cuda:0") for x in (a, p, o))
+    from fractions import Fraction
+    for M in (w.M_kv, 0):
+        for al in w.alphas:
+            kw = dict(B=w.B, alpha=al, M_kv=M)
+            raw, _, _ = fs.simulate(ta, tp, to, policy="isjl", cost_c=0, cost_tau=1, **kw)
+            torch.cuda.synchronize()
+            Ti = fs.metrics_view(raw)["T"].copy()
+            ms_sim = _median_launch_ms(torch, lambda: fs.simulate(ta, tp, to, policy="isjl",
+                                                                  **kw))
+            To, _ = fs.bruteforce_opt(ta, tp, to, **kw)
+            torch.cuda.synchronize()
+            To = To.cpu().numpy()
+            t0 = time.perf_counter()
+            fs.bruteforce_opt(ta, tp, to, **kw)
+            torch.cuda.synchronize()
+            s_opt = time.perf_counter() - t0
+            # makespans are below 2^8 here, so distinct ratios differ by far more than
+            # a double's rounding: the argmin of the doubles is an exact minimum
+            k = int(np.argmin(To / Ti))
+            worst = Fraction(int(To[k]), int(Ti[k]))
+            c0 = time.perf_counter()
+            oracle.opt(a[:64], p[:64], o[:64], **kw)
+            one = max((time.perf_counter() - c0) / 64, 1e-6)
+            k1 = int(max(64, secs / 2 / one))
+            c0 = time.perf_counter()
+            r1 = oracle.opt(a[:k1], p[:k1], o[:k1], **kw)
+            s1 = time.perf_counter() - c0
+            kn = k1 * threads
+            c0 = time.perf_counter()
+            rn = oracle.opt_parallel(a[:kn], p[:kn], o[:kn], threads=threads, **kw)
+            sn = time.perf_counter() - c0
+            row = {"workload": w.name, "policy": "isjl+opt", "alpha": al, "M_kv": M,
+                   "sum_T_isjl": int(Ti.sum()), "gpu_isjl_instance_steps_per_s":
+                   float(Ti.sum()) / (ms_sim / 1e3), "gpu_opt_solves_per_s": w.n_inst / s_opt,
+                   "oracle_opt_1core_solves_per_s": k1 / s1,
+                   "oracle_opt_all_cores_solves_per_s": kn / sn, "oracle_threads": threads,
+                   "min_T_opt_over_T_isjl": f"{worst.numerator}/{worst.denominator}",
+                   "parity_on_samples": bool((r1 == To[:k1]).all() and (rn == To[:kn]).all())}
+            print(json.dumps(row), file=sys.stderr, flush=True)
+            rows.append(row)
+    print(json.dumps({"mode": "configs", "cpu_model": cpu_model(), "nproc": os.cpu_count(),
+                      "rows": rows}))
     return 0
 
 

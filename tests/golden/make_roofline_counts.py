@@ -31,8 +31,14 @@ import oracle  # noqa: E402
 import workload  # noqa: E402
 
 SAMPLE = 128
+INF = oracle.ALPHA_INF
 RUNS = [("pareto_65536x2000", "isjl", 128)] + [
-    ("bimodal_sweep_4096x2000", "isjl", al) for al in (0, 16, 64, 256, 1024, oracle.ALPHA_INF)]
+    ("bimodal_sweep_4096x2000", "isjl", al) for al in (0, 16, 64, 256, 1024, INF)] + [
+    ("bimodal_sweep_4096x2000", "fcfs", INF), ("bimodal_sweep_4096x2000", "ljf", 64),
+    ("uniform_256x64", "fcfs", INF), ("uniform_256x64", "ljf", 8), ("uniform_256x64", "isjl", 8),
+    ("lognormal_4096x1000", "fcfs", INF), ("lognormal_4096x1000", "ljf", 64),
+    ("lognormal_4096x1000", "isjl", 64)] + [
+    ("tiny_opt_1048576x8", "isjl", al) for al in (1, 2, 4)]
 
 
 def event_wave_ops(start, finish):
