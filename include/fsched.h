@@ -224,10 +224,15 @@ int fsched_cost_decompose(const fsched_params* p, int64_t n_inst, int32_t n_jobs
  * reservations within M_kv unless a job runs alone, and |s_i - s_j| <= alpha for
  * every pair active at a common step.  Exhaustive search over schedules in start
  * order with a memo and lower bounds, started from the ISJL schedule of the
- * instance (which is returned when nothing beats it).  The search of one
- * instance is capped at 2^22 steps; an instance that reaches the cap gets
- * T_opt = FSCHED_T_INTERNAL (host mode: EINTERNAL).  No instance of the tiny
- * workloads at B <= 3 comes near it; at B = 4 a few do.
+ * instance (which is returned when nothing beats it).  A first pass keeps the
+ * search's memo in LDS and stops a search after 2^22 steps; the searches it
+ * stops are run again by a second pass with a memo of 2^20 entries per wave in
+ * device scratch (256 MiB from the library's pool, with the instance list;
+ * stream-ordered, released after the call) and a cap of 2^28 steps.  Only a
+ * search past that cap gets T_opt = FSCHED_T_INTERNAL (host mode: EINTERNAL);
+ * on the tiny workload (4,096 instances, B = 3 and 4, alpha up to 19, with and
+ * without a KV budget) none does.  If the scratch cannot be had, the second
+ * pass is skipped and the searches the first pass stopped get the marker.
  *   n_jobs     <= 8 (ETOOLARGE otherwise); every length <= 255 and every
  *              arrival <= 4095 (else T = FSCHED_T_TOOLARGE / ETOOLARGE).
  *   T_opt      [n_inst] int64 optimum makespan.

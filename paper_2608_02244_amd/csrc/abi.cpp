@@ -527,6 +527,25 @@ int fsched_bruteforce_opt(const fsched_params* p, int64_t n_inst, int32_t n_jobs
   a.wave_words = (int32_t)fs::opt_lds_words_per_wave();
   const int wpb = 1;
   const size_t lds = (size_t)a.wave_words * 4 * wpb;
+  // Scratch of the second pass (searches the first pass's LDS memo could not
+  // finish): the list of their instances, two counters and a memo region per
+  // wave, from the library's pool (else the device's default pool).
+  const size_t list_bytes = round256((size_t)n_inst * 4 + 8);
+  const size_t memo_bytes = (size_t)fs::OPT_FB_WAVES * fs::OPT_FB_MEMO_ENTRIES * 16;
+  void* fb = nullptr;
+  {
+    hipMemPool_t pool = rank_pool();
+    hipError_t e = pool ? hipMallocFromPoolAsync(&fb, list_bytes + memo_bytes, pool, s)
+                        : hipErrorNotSupported;
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      fb = nullptr;
+      if (hipMallocAsync(&fb, list_bytes + memo_bytes, s) != hipSuccess) {
+        (void)hipGetLastError();
+        fb = nullptr;  // no second pass: a capped search reports FSCHED_T_INTERNAL
+      }
+    }
+  }
   auto run = [&](const int32_t* da, const int32_t* dp, const int32_t* dq, int64_t* dT,
                  int32_t* dS) -> int {
     int r = launch_simulate(&sp, n_inst, n_jobs, da, dp, dq, nullptr, dT, dS, nullptr, s);
@@ -536,11 +555,24 @@ int fsched_bruteforce_opt(const fsched_params* p, int64_t n_inst, int32_t n_jobs
     a.output = dq;
     a.T = dT;
     a.start = dS;
+    if (fb) {
+      a.fb_count = (int32_t*)fb;
+      a.fb_list = (int32_t*)fb + 2;
+      a.fb_memo = (uint32_t*)((char*)fb + list_bytes);
+      hipError_t e = hipMemsetAsync(a.fb_count, 0, 8, s);
+      if (e != hipSuccess) return hip_fail(e);
+    }
     hipError_t e = fs::launch_opt(a, wpb, lds, s);
+    if (e == hipSuccess && fb)
+      e = fs::launch_opt_fallback(a, fs::opt_fallback_lds_words_per_wave() * 4, s);
     return e == hipSuccess ? FSCHED_OK : hip_fail(e);
+  };
+  auto release_fb = [&]() {
+    if (fb && hipFreeAsync(fb, s) != hipSuccess) (void)hipGetLastError();
   };
   if (p->flags & FSCHED_F_DEVICE_PTRS) {
     rc = run(arrival, prompt, output, T_opt, start_opt);
+    release_fb();
     if (rc) return rc;
     if (p->flags & FSCHED_F_SYNC) {
       hipError_t e = hipStreamSynchronize(s);
@@ -555,8 +587,12 @@ int fsched_bruteforce_opt(const fsched_params* p, int64_t n_inst, int32_t n_jobs
   const int32_t* dq = (const int32_t*)st.upload(output, tb);
   int64_t* dT = (int64_t*)st.alloc((size_t)n_inst * sizeof(int64_t));
   int32_t* dS = start_opt ? (int32_t*)st.alloc(tb) : nullptr;
-  if (st.err != hipSuccess) return hip_fail(st.err);
+  if (st.err != hipSuccess) {
+    release_fb();
+    return hip_fail(st.err);
+  }
   rc = run(da, dp, dq, dT, dS);
+  release_fb();
   if (rc) return rc;
   hipError_t e = hipStreamSynchronize(s);
   if (e == hipSuccess)

@@ -37,14 +37,12 @@ namespace fs {
 namespace {
 
 constexpr int NMAX = 8;
-constexpr int MEMO_BYTES = 32768;     // memo bytes per wave
-constexpr int MEMO_W = MEMO_BYTES / 16;  // general layout: 4 words per entry
-constexpr int MEMO_C = MEMO_BYTES / 8;   // compact layout: one 64-bit word per entry
+constexpr int MEMO_BYTES = 32768;     // LDS memo bytes per wave (first pass)
 constexpr int FRAMES = NMAX + 2;      // DFS depth <= n, plus the root
 constexpr int FW = 8;                 // words per frame
 constexpr int CACHE = 192;            // cached candidate keys per frame (3 per lane)
 constexpr uint32_t NOKEY = 0xFFFFFFFFu;
-constexpr int GUARD = 1 << 22;        // DFS pushes per search before giving up
+constexpr int GUARD = 1 << 22;        // DFS pushes per search in the first pass
 
 // frame word offsets
 enum { F_S = 0, F_SIG, F_PLO, F_PHI, F_BOUND, F_BEST, F_THR, F_FLAGS };
@@ -137,9 +135,29 @@ __device__ __forceinline__ uint32_t mix(uint32_t k0, uint32_t k1, uint32_t k2) {
   return h;
 }
 
+// The memo: a hash table probed 64 slots at a time.  The first pass keeps it in
+// LDS; the second pass in its own region of global scratch, read and written
+// with agent-scope accesses (they bypass the vector L1, so a lane reads what
+// another lane of the wave stored).
 struct Memo {
   uint32_t* base;
-  bool compact;
+  bool compact;  // one 64-bit word per entry (LDS only), else 4 words per entry
+  bool global;
+  int entries;   // power of two
+
+  __device__ uint32_t ld(const uint32_t* p) const {
+    if (global) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return *p;
+  }
+  __device__ void st(uint32_t* p, uint32_t v) const {
+    if (global) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else *p = v;
+  }
+  // every lane sees the stores of the wave before its next probe
+  __device__ void sync() const {
+    if (global) __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "agent");
+    wave_lds_sync();
+  }
 
   // Compact key: valid | S | up to three active (index, progress) pairs in index order.
   __device__ static uint64_t ckey(uint32_t S, uint32_t plo, uint32_t phi) {
@@ -163,7 +181,7 @@ struct Memo {
       const uint64_t key = ckey(S, b, c);
       const uint64_t* T = (const uint64_t*)base;
       const uint32_t h = mix((uint32_t)(key >> 32), (uint32_t)key, 0u);
-      const int slot = (int)((h + (uint32_t)lane) & (MEMO_C - 1));
+      const int slot = (int)((h + (uint32_t)lane) & (uint32_t)(entries - 1));
       const uint64_t x = T[slot];
       const bool hit = (x >> 16) == (key >> 16);
       const bool empty = x == 0ull;
@@ -174,20 +192,20 @@ struct Memo {
       const uint32_t v = (uint32_t)readlane((int)(uint32_t)(x & 0xFFFFu), L);
       return (v & 0x7FFFu) | ((v & 0x8000u) << 16);
     }
-    uint32_t* k0 = base;
-    uint32_t* k1 = base + MEMO_W;
-    uint32_t* k2 = base + 2 * MEMO_W;
-    uint32_t* val = base + 3 * MEMO_W;
+    const uint32_t* k0 = base;
+    const uint32_t* k1 = base + entries;
+    const uint32_t* k2 = base + 2 * (size_t)entries;
+    const uint32_t* val = base + 3 * (size_t)entries;
     const uint32_t h = mix(a, b, c);
-    const int slot = (int)((h + (uint32_t)lane) & (MEMO_W - 1));
-    const uint32_t x = k0[slot];
-    const bool hit = x == a && k1[slot] == b && k2[slot] == c;
+    const int slot = (int)((h + (uint32_t)lane) & (uint32_t)(entries - 1));
+    const uint32_t x = ld(k0 + slot);
+    const bool hit = x == a && ld(k1 + slot) == b && ld(k2 + slot) == c;
     const bool empty = x == 0u;
     const uint64_t mh = ballot(hit), me = ballot(empty);
     if (!mh) return NOKEY;
     const int L = __builtin_ctzll(mh);
     if (me && __builtin_ctzll(me) < L) return NOKEY;  // keys sit before any hole
-    return (uint32_t)readlane((int)val[slot], L);
+    return (uint32_t)readlane((int)ld(val + slot), L);
   }
 
   __device__ void put(uint32_t a, uint32_t b, uint32_t c, uint32_t S, uint32_t v, int lane) {
@@ -195,7 +213,7 @@ struct Memo {
       const uint64_t key = ckey(S, b, c);
       uint64_t* T = (uint64_t*)base;
       const uint32_t h = mix((uint32_t)(key >> 32), (uint32_t)key, 0u);
-      const int slot = (int)((h + (uint32_t)lane) & (MEMO_C - 1));
+      const int slot = (int)((h + (uint32_t)lane) & (uint32_t)(entries - 1));
       const uint64_t x = T[slot];
       const bool hit = (x >> 16) == (key >> 16);
       const bool empty = x == 0ull;
@@ -207,13 +225,13 @@ struct Memo {
       return;
     }
     uint32_t* k0 = base;
-    uint32_t* k1 = base + MEMO_W;
-    uint32_t* k2 = base + 2 * MEMO_W;
-    uint32_t* val = base + 3 * MEMO_W;
+    uint32_t* k1 = base + entries;
+    uint32_t* k2 = base + 2 * (size_t)entries;
+    uint32_t* val = base + 3 * (size_t)entries;
     const uint32_t h = mix(a, b, c);
-    const int slot = (int)((h + (uint32_t)lane) & (MEMO_W - 1));
-    const uint32_t x = k0[slot];
-    const bool hit = x == a && k1[slot] == b && k2[slot] == c;
+    const int slot = (int)((h + (uint32_t)lane) & (uint32_t)(entries - 1));
+    const uint32_t x = ld(k0 + slot);
+    const bool hit = x == a && ld(k1 + slot) == b && ld(k2 + slot) == c;
     const bool empty = x == 0u;
     const uint64_t mh = ballot(hit), me = ballot(empty);
     int L;
@@ -221,17 +239,18 @@ struct Memo {
     else if (me) L = __builtin_ctzll(me);
     else L = 0;  // probe window full: replace the home slot
     if (lane == L) {
-      k0[slot] = a;
-      k1[slot] = b;
-      k2[slot] = c;
-      val[slot] = v;
+      st(k0 + slot, a);
+      st(k1 + slot, b);
+      st(k2 + slot, c);
+      st(val + slot, v);
     }
-    wave_lds_sync();
+    sync();
   }
 
   __device__ void clear(int lane) {
-    for (int i = lane; i < MEMO_BYTES / 4; i += WAVE) base[i] = 0u;
-    wave_lds_sync();
+    const size_t words = compact ? 2 * (size_t)entries : 4 * (size_t)entries;
+    for (size_t i = (size_t)lane; i < words; i += WAVE) st(base + i, 0u);
+    sync();
   }
 };
 
@@ -288,8 +307,10 @@ struct Dfs {
     return wave_umin(best);
   }
 
-  // V(root) if it is below `bound`, else a value >= bound; -1 if the push guard trips.
-  __device__ int run(uint32_t S0, int sig0, uint32_t plo0, uint32_t phi0, int bound0) {
+  // V(root) if it is below `bound`, else a value >= bound; -1 after more than
+  // `guard_max` pushes.
+  __device__ int run(uint32_t S0, int sig0, uint32_t plo0, uint32_t phi0, int bound0,
+                     int guard_max) {
     int depth = 0;
     set(0, F_S, S0);
     set(0, F_SIG, (uint32_t)sig0);
@@ -363,7 +384,7 @@ struct Dfs {
           set(depth + 1, F_FLAGS, 0u);
           wave_lds_sync();
           depth++;
-          if (++guard > GUARD) return -1;  // the cap: some 8-job searches at B = 4 reach it
+          if (++guard > guard_max) return -1;
           continue;
         }
         memo.put(ka, plo, phi, S, (uint32_t)best | ((best < bound) ? 0x80000000u : 0u), lane);
@@ -380,21 +401,10 @@ struct Dfs {
   }
 };
 
-}  // namespace
-
-__global__ __launch_bounds__(256) void opt_kernel(OptArgs a) {
-  extern __shared__ uint32_t lds_raw[];
-  const int wib = threadIdx.x >> 6;
-  const int64_t inst = (int64_t)blockIdx.x * (blockDim.x >> 6) + wib;
-  if (inst >= a.n_inst) return;
-  const int lane = lane_id();
-  uint32_t* base = lds_raw + (size_t)wib * (size_t)a.wave_words;
-  uint32_t* frames = base + MEMO_BYTES / 4;
-  uint32_t* keys = frames + FRAMES * FW;
-
+// Read instance `inst` into I.  False (after writing the marker) when a length
+// or an arrival is beyond the search's limits.
+__device__ bool load_inst(const OptArgs& a, int64_t inst, int lane, Inst& I) {
   const int n = a.n;
-  const int64_t ub = a.T[inst];  // ISJL makespan (or an error marker)
-  if (ub < 0) return;
   const int64_t row = inst * (int64_t)n;
   int lv = 0, av = 0, bad = 0;
   if (lane < n) {
@@ -404,9 +414,8 @@ __global__ __launch_bounds__(256) void opt_kernel(OptArgs a) {
   }
   if (ballot(bad != 0)) {
     if (lane == 0) a.T[inst] = FSCHED_T_TOOLARGE;
-    return;
+    return false;
   }
-  Inst I;
   I.n = n;
   I.B = a.B;
   I.alpha = a.alpha;
@@ -438,21 +447,24 @@ __global__ __launch_bounds__(256) void opt_kernel(OptArgs a) {
     I.compat[j] = c;
   }
   I.compact = I.B <= 3 && I.rmax == 0;
-  Memo memo{base, I.compact};
-  memo.clear(lane);
+  return true;
+}
 
+// Search instance `inst` below its incumbent (the ISJL makespan in T) and, when
+// something better exists, write the optimum and one optimal schedule.  False
+// if the search made more than `guard_max` pushes (nothing written then).
+__device__ bool solve(const OptArgs& a, int64_t inst, const Inst& I, Memo& memo, uint32_t* frames,
+                      uint32_t* keys, int lane, int guard_max) {
+  const int64_t row = inst * (int64_t)a.n;
   Dfs dfs{I, memo, frames, keys, lane};
   const uint32_t none = 0xFFFFFFFFu;
-  const int bound = (int)ub;
-  const int v = dfs.run(0u, 0, none, none, bound);
-  if (v < 0) {
-    if (lane == 0) a.T[inst] = FSCHED_T_INTERNAL;
-    return;
-  }
-  if (v >= bound) return;  // ISJL's schedule (already written) is optimal
+  const int bound = (int)a.T[inst];
+  const int v = dfs.run(0u, 0, none, none, bound, guard_max);
+  if (v < 0) return false;
+  if (v >= bound) return true;  // ISJL's schedule (already written) is optimal
 
   if (lane == 0) a.T[inst] = v;
-  if (!a.start) return;
+  if (!a.start) return true;
   // Reconstruct one optimal schedule: from each state take the first candidate
   // (in key order) whose child reaches the state's value.
   uint32_t S = 0u, plo = none, phi = none;
@@ -480,7 +492,7 @@ __global__ __launch_bounds__(256) void opt_kernel(OptArgs a) {
         if (j < 4) nlo |= (uint32_t)q << (8 * j);
         else nhi |= (uint32_t)q << (8 * (j - 4));
       }
-      const int cv = dfs.run(S | (1u << k), sig + d, nlo, nhi, val - d + 1);
+      const int cv = dfs.run(S | (1u << k), sig + d, nlo, nhi, val - d + 1, guard_max);
       if (cv >= 0 && cv + d == val) {
         if (lane == 0) a.start[row + k] = sig + d;
         S |= 1u << k;
@@ -494,6 +506,63 @@ __global__ __launch_bounds__(256) void opt_kernel(OptArgs a) {
     }
     if (!moved) break;  // not reachable: some child always attains the value
   }
+  return true;
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(256) void opt_kernel(OptArgs a) {
+  extern __shared__ uint32_t lds_raw[];
+  const int wib = threadIdx.x >> 6;
+  const int64_t inst = (int64_t)blockIdx.x * (blockDim.x >> 6) + wib;
+  if (inst >= a.n_inst) return;
+  const int lane = lane_id();
+  uint32_t* base = lds_raw + (size_t)wib * (size_t)a.wave_words;
+  uint32_t* frames = base + MEMO_BYTES / 4;
+  uint32_t* keys = frames + FRAMES * FW;
+
+  if (a.T[inst] < 0) return;  // ISJL's error marker
+  Inst I;
+  if (!load_inst(a, inst, lane, I)) return;
+  Memo memo{base, I.compact, false, I.compact ? MEMO_BYTES / 8 : MEMO_BYTES / 16};
+  memo.clear(lane);
+  if (!solve(a, inst, I, memo, frames, keys, lane, GUARD)) {
+    // the LDS memo was too small for this search: leave it to the second pass
+    if (lane == 0) {
+      if (a.fb_list) {
+        const int slot = atomicAdd(a.fb_count, 1);
+        a.fb_list[slot] = (int32_t)inst;
+      } else {
+        a.T[inst] = FSCHED_T_INTERNAL;
+      }
+    }
+  }
+}
+
+// Second pass: OPT_FB_WAVES persistent waves take the listed instances one at a
+// time (claimed with an atomic counter) and search them again with a memo of
+// OPT_FB_MEMO_ENTRIES entries in their own region of global scratch.  Every
+// wave leaves once the list is exhausted.
+__global__ __launch_bounds__(64) void opt_fallback_kernel(OptArgs a) {
+  extern __shared__ uint32_t lds_raw[];
+  const int lane = lane_id();
+  uint32_t* frames = lds_raw;
+  uint32_t* keys = frames + FRAMES * FW;
+  const int nlist = __hip_atomic_load(a.fb_count, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  Memo memo{a.fb_memo + (size_t)blockIdx.x * 4 * (size_t)OPT_FB_MEMO_ENTRIES, false, true,
+            OPT_FB_MEMO_ENTRIES};
+  while (true) {
+    int idx = 0;
+    if (lane == 0) idx = atomicAdd(a.fb_count + 1, 1);
+    idx = readlane(idx, 0);
+    if (idx >= nlist) break;
+    const int64_t inst = a.fb_list[idx];
+    Inst I;
+    if (!load_inst(a, inst, lane, I)) continue;
+    memo.clear(lane);
+    if (!solve(a, inst, I, memo, frames, keys, lane, OPT_FB_GUARD))
+      if (lane == 0) a.T[inst] = FSCHED_T_INTERNAL;
+  }
 }
 
 hipError_t launch_opt(const OptArgs& a, int wpb, size_t lds, hipStream_t s) {
@@ -502,6 +571,14 @@ hipError_t launch_opt(const OptArgs& a, int wpb, size_t lds, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t launch_opt_fallback(const OptArgs& a, size_t lds, hipStream_t s) {
+  hipLaunchKernelGGL(opt_fallback_kernel, dim3((unsigned)OPT_FB_WAVES), dim3((unsigned)WAVE), lds,
+                     s, a);
+  return hipGetLastError();
+}
+
 size_t opt_lds_words_per_wave() { return MEMO_BYTES / 4 + FRAMES * FW + FRAMES * CACHE; }
+
+size_t opt_fallback_lds_words_per_wave() { return FRAMES * FW + FRAMES * CACHE; }
 
 }  // namespace fs

@@ -131,3 +131,27 @@ def test_tiny_opt_workload_full_size(dev, M_kv):
         assert np.array_equal(Tn[sample], ref)
         r = Tn / Ti
         log(f"  min T_opt/T_isjl = {r.min():.4f} at instance {int(r.argmin())}")
+
+
+# Instances of the tiny workload (first 4,096) whose search fills the first
+# pass's LDS memo before it ends (B = 3 or 4, large alpha): the second pass with
+# its large memo must finish them, at the oracle's optimum.
+CAPPED = [(4, 0, 11, 158), (4, 0, 11, 862), (4, 0, 11, 3430), (4, 0, 15, 1189),
+          (3, 0, 15, 2273), (4, 16, 11, 1504), (4, 16, 11, 1508)]
+
+
+def test_searches_beyond_the_first_pass_cap(dev):
+    import torch
+    a, p, o = workload.generate("tiny_opt_1048576x8", n_inst=4096)
+    for B, M, al, i in CAPPED:
+        ctx = f"instance {i} B={B} M_kv={M} alpha={al}"
+        log(ctx)
+        t = [torch.from_numpy(x[i:i + 1].copy()).to(dev) for x in (a, p, o)]
+        T, st = fs.bruteforce_opt(*t, B=B, alpha=al, M_kv=M, schedule=True)
+        torch.cuda.synchronize()
+        T = T.cpu().numpy()
+        ref = oracle.opt(a[i:i + 1], p[i:i + 1], o[i:i + 1], B=B, alpha=al, M_kv=M)
+        assert int(T[0]) == int(ref[0]), f"{ctx}: gpu {int(T[0])} oracle {int(ref[0])}"
+        m, v = oracle.decompose(a[i:i + 1], p[i:i + 1], o[i:i + 1], st.cpu().numpy(), B=B,
+                                alpha=al, M_kv=M)
+        assert int(v[0]) == 0 and int(m["T"][0]) == int(T[0]), ctx
