@@ -17,11 +17,12 @@ namespace fs {
 // with p ^ d for d = size/4 .. 1; the lower position keeps the minimum.
 template <int M>
 __device__ __forceinline__ int shfl_mirror_c(int v) {
-  // value of lane (lane ^ M), M = 2^j - 1
-  if constexpr (M == 1) return dpp<DPP_QP_XOR1>(v, v);
-  else if constexpr (M == 3) return dpp<0x1B>(v, v);  // quad_perm [3,2,1,0]
-  else if constexpr (M == 7) return dpp<DPP_HALF_MIRROR>(v, v);
-  else if constexpr (M == 15) return dpp<DPP_MIRROR>(v, v);
+  // value of lane (lane ^ M), M = 2^j - 1 (every lane's source is valid, so
+  // the DPP forms leave "old" undefined and fuse into their consumers)
+  if constexpr (M == 1) return dpp_perm<DPP_QP_XOR1>(v);
+  else if constexpr (M == 3) return dpp_perm<0x1B>(v);  // quad_perm [3,2,1,0]
+  else if constexpr (M == 7) return dpp_perm<DPP_HALF_MIRROR>(v);
+  else if constexpr (M == 15) return dpp_perm<DPP_MIRROR>(v);
   else if constexpr (M == 31) return __builtin_amdgcn_ds_swizzle(v, (31 << 10) | 0x1F);
   else return __shfl_xor(v, 63);
 }

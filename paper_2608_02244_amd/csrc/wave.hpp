@@ -36,6 +36,14 @@ __device__ __forceinline__ int dpp(int old, int src) {
   return __builtin_amdgcn_update_dpp(old, src, CTRL, ROW_MASK, BANK_MASK, BOUND);
 }
 
+// DPP permutation of v in which every lane's source lane is valid (quad
+// permutes, mirrors, row rotates): no "old" value is needed, so the move can
+// fuse into the instructions that consume it.
+template <int CTRL>
+__device__ __forceinline__ int dpp_perm(int v) {
+  return __builtin_amdgcn_mov_dpp(v, CTRL, 0xf, 0xf, true);
+}
+
 // quad_perm [1,0,3,2], [2,3,0,1]; row_half_mirror; row_mirror; row_bcast15; row_bcast31
 enum : int {
   DPP_QP_XOR1 = 0xB1,
@@ -52,35 +60,41 @@ enum : int {
 };
 
 // Reductions: after the butterfly inside each row of 16 every lane holds its
-// row's value; the two broadcasts fold rows 0..3 into lanes 48..63.
+// row's value; the two broadcasts fold rows 0..3 into lanes 48..63.  The DPP
+// moves take the operation's identity as their "old" value (every lane read
+// here has a valid source, and rows outside a broadcast's row mask are not
+// written), which lets the compiler fuse each move into the min / max itself.
 __device__ __forceinline__ int wave_min(int v) {
-  v = min(v, dpp<DPP_QP_XOR1>(v, v));
-  v = min(v, dpp<DPP_QP_XOR2>(v, v));
-  v = min(v, dpp<DPP_HALF_MIRROR>(v, v));
-  v = min(v, dpp<DPP_MIRROR>(v, v));
-  v = min(v, dpp<DPP_BCAST15, 0xa>(v, v));
-  v = min(v, dpp<DPP_BCAST31, 0xc>(v, v));
+  constexpr int ID = 0x7FFFFFFF;
+  v = min(v, dpp<DPP_QP_XOR1>(ID, v));
+  v = min(v, dpp<DPP_QP_XOR2>(ID, v));
+  v = min(v, dpp<DPP_HALF_MIRROR>(ID, v));
+  v = min(v, dpp<DPP_MIRROR>(ID, v));
+  v = min(v, dpp<DPP_BCAST15, 0xa>(ID, v));
+  v = min(v, dpp<DPP_BCAST31, 0xc>(ID, v));
   return readlane(v, 63);
 }
 
 __device__ __forceinline__ int wave_max(int v) {
-  v = max(v, dpp<DPP_QP_XOR1>(v, v));
-  v = max(v, dpp<DPP_QP_XOR2>(v, v));
-  v = max(v, dpp<DPP_HALF_MIRROR>(v, v));
-  v = max(v, dpp<DPP_MIRROR>(v, v));
-  v = max(v, dpp<DPP_BCAST15, 0xa>(v, v));
-  v = max(v, dpp<DPP_BCAST31, 0xc>(v, v));
+  constexpr int ID = (int)0x80000000;
+  v = max(v, dpp<DPP_QP_XOR1>(ID, v));
+  v = max(v, dpp<DPP_QP_XOR2>(ID, v));
+  v = max(v, dpp<DPP_HALF_MIRROR>(ID, v));
+  v = max(v, dpp<DPP_MIRROR>(ID, v));
+  v = max(v, dpp<DPP_BCAST15, 0xa>(ID, v));
+  v = max(v, dpp<DPP_BCAST31, 0xc>(ID, v));
   return readlane(v, 63);
 }
 
 __device__ __forceinline__ uint32_t wave_umin(uint32_t v) {
+  constexpr int ID = (int)0xFFFFFFFFu;
   int x = (int)v;
-  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_QP_XOR1>(x, x));
-  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_QP_XOR2>(x, x));
-  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_HALF_MIRROR>(x, x));
-  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_MIRROR>(x, x));
-  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_BCAST15, 0xa>(x, x));
-  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_BCAST31, 0xc>(x, x));
+  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_QP_XOR1>(ID, x));
+  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_QP_XOR2>(ID, x));
+  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_HALF_MIRROR>(ID, x));
+  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_MIRROR>(ID, x));
+  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_BCAST15, 0xa>(ID, x));
+  x = (int)min((uint32_t)x, (uint32_t)dpp<DPP_BCAST31, 0xc>(ID, x));
   return (uint32_t)readlane(x, 63);
 }
 
@@ -142,9 +156,9 @@ __device__ __forceinline__ int wave_scan_incl_min(int x) {
 template <int D>
 __device__ __forceinline__ int shfl_xor_c(int v) {
   static_assert(D > 0 && D < WAVE && (D & (D - 1)) == 0, "xor distance");
-  if constexpr (D == 1) return dpp<DPP_QP_XOR1>(v, v);
-  else if constexpr (D == 2) return dpp<DPP_QP_XOR2>(v, v);
-  else if constexpr (D == 8) return dpp<0x128>(v, v);  // row_ror:8
+  if constexpr (D == 1) return dpp_perm<DPP_QP_XOR1>(v);
+  else if constexpr (D == 2) return dpp_perm<DPP_QP_XOR2>(v);
+  else if constexpr (D == 8) return dpp_perm<0x128>(v);  // row_ror:8
   else if constexpr (D == 4 || D == 16) return __builtin_amdgcn_ds_swizzle(v, (D << 10) | 0x1F);
   else return __shfl_xor(v, D);
 }
