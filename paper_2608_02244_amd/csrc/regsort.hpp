@@ -78,8 +78,50 @@ __device__ __forceinline__ void lm_half_lanes(uint32_t (&key)[KS], int lane) {
   }
 }
 
+// The same two lane stages, each key taking its half of the exchange with a
+// median of three: with c = 0 it is min(a, b) and with c = ~0u max(a, b), c
+// chosen per lane.  One instruction fewer per key, but a DPP partner then
+// needs a register of its own instead of fusing into the min and the max:
+// taken by the re-scoring kernel, not by the simulation kernels, which are at
+// their register limits.
+__device__ __forceinline__ uint32_t umed3(uint32_t a, uint32_t b, uint32_t c) {
+  return max(min(a, b), min(max(a, b), c));
+}
+
+template <int M, int KS>
+__device__ __forceinline__ void lm3_mirror_lanes(uint32_t (&key)[KS], int lane) {
+  const uint32_t side = (lane & ((M + 1) >> 1)) == 0 ? 0u : ~0u;  // lower lanes keep the min
+#pragma unroll
+  for (int k = 0; k < KS / 2 + (KS & 1); ++k) {
+    const int h = KS - 1 - k;
+    const uint32_t a = key[k], b = key[h];
+    const uint32_t pa = (uint32_t)shfl_mirror_c<M>((int)b);
+    if (h != k) key[h] = umed3(b, (uint32_t)shfl_mirror_c<M>((int)a), side);
+    key[k] = umed3(a, pa, side);
+  }
+}
+
+template <int D, int KS>
+__device__ __forceinline__ void lm3_half_lanes(uint32_t (&key)[KS], int lane) {
+  const uint32_t side = (lane & D) == 0 ? 0u : ~0u;  // lower lanes keep the min
+#pragma unroll
+  for (int k = 0; k < KS; ++k) key[k] = umed3(key[k], (uint32_t)shfl_xor_c<D>((int)key[k]), side);
+}
+
+template <int M, int KS, bool MED3>
+__device__ __forceinline__ void mirror_lanes(uint32_t (&key)[KS], int lane) {
+  if constexpr (MED3) lm3_mirror_lanes<M>(key, lane);
+  else lm_mirror_lanes<M>(key, lane);
+}
+
+template <int D, int KS, bool MED3>
+__device__ __forceinline__ void half_lanes(uint32_t (&key)[KS], int lane) {
+  if constexpr (MED3) lm3_half_lanes<D>(key, lane);
+  else lm_half_lanes<D>(key, lane);
+}
+
 // Sort the 64 * KS keys held in registers, ascending in lane-major order.
-template <int KS>
+template <int KS, bool MED3 = false>
 __device__ inline void reg_sort_keys(uint32_t (&key)[KS], int lane) {
   for (int size = 2; size <= KS * WAVE; size <<= 1) {
     if (size <= KS) {
@@ -93,12 +135,12 @@ __device__ inline void reg_sort_keys(uint32_t (&key)[KS], int lane) {
       }
     } else {
       switch (size / KS) {
-        case 2: lm_mirror_lanes<1>(key, lane); break;
-        case 4: lm_mirror_lanes<3>(key, lane); break;
-        case 8: lm_mirror_lanes<7>(key, lane); break;
-        case 16: lm_mirror_lanes<15>(key, lane); break;
-        case 32: lm_mirror_lanes<31>(key, lane); break;
-        default: lm_mirror_lanes<63>(key, lane); break;
+        case 2: mirror_lanes<1, KS, MED3>(key, lane); break;
+        case 4: mirror_lanes<3, KS, MED3>(key, lane); break;
+        case 8: mirror_lanes<7, KS, MED3>(key, lane); break;
+        case 16: mirror_lanes<15, KS, MED3>(key, lane); break;
+        case 32: mirror_lanes<31, KS, MED3>(key, lane); break;
+        default: mirror_lanes<63, KS, MED3>(key, lane); break;
       }
     }
     for (int d = size >> 2; d > 0; d >>= 1) {
@@ -113,12 +155,12 @@ __device__ inline void reg_sort_keys(uint32_t (&key)[KS], int lane) {
         }
       } else {
         switch (d / KS) {
-          case 1: lm_half_lanes<1>(key, lane); break;
-          case 2: lm_half_lanes<2>(key, lane); break;
-          case 4: lm_half_lanes<4>(key, lane); break;
-          case 8: lm_half_lanes<8>(key, lane); break;
-          case 16: lm_half_lanes<16>(key, lane); break;
-          default: lm_half_lanes<32>(key, lane); break;
+          case 1: half_lanes<1, KS, MED3>(key, lane); break;
+          case 2: half_lanes<2, KS, MED3>(key, lane); break;
+          case 4: half_lanes<4, KS, MED3>(key, lane); break;
+          case 8: half_lanes<8, KS, MED3>(key, lane); break;
+          case 16: half_lanes<16, KS, MED3>(key, lane); break;
+          default: half_lanes<32, KS, MED3>(key, lane); break;
         }
       }
     }
@@ -188,12 +230,12 @@ __device__ inline void reg_sort_payload(uint32_t (&key)[KS], int (&val)[KS], int
 
 // Sort W[0 .. 64*KS) ascending through registers (W is read in any order and
 // written back sorted).
-template <int KS>
+template <int KS, bool MED3 = false>
 __device__ inline void wave_reg_sort(uint32_t* W, int lane) {
   uint32_t key[KS];
 #pragma unroll
   for (int k = 0; k < KS; ++k) key[k] = W[k * WAVE + lane];
-  reg_sort_keys<KS>(key, lane);
+  reg_sort_keys<KS, MED3>(key, lane);
   wave_lds_sync();
 #pragma unroll
   for (int k = 0; k < KS; ++k) W[lane * KS + k] = key[k];

@@ -57,6 +57,7 @@ enum : int {
   DPP_ROW_SHR3 = 0x113,
   DPP_ROW_SHR4 = 0x114,
   DPP_ROW_SHR8 = 0x118,
+  DPP_WAVE_SHL1 = 0x130,  // lane i reads lane i + 1 (lane 63 keeps the old value)
 };
 
 // Reductions: after the butterfly inside each row of 16 every lane holds its
