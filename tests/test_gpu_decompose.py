@@ -173,3 +173,33 @@ def test_long_jobs_take_the_wide_pass(dev):
         same(f"long jobs {kw}", got, ref, gv, rv)
         hm, hv = fs.cost_decompose(a, p, o, s, **kw)
         same(f"long jobs host mode {kw}", hm, ref, hv, rv)
+
+
+def test_start_groups_across_chunks(dev):
+    """Schedules built from few start times and few lengths: groups of up to
+    hundreds of simultaneous starts and ends that span several 64-event chunks,
+    the earliest and the latest active start losing their last job at any
+    position of a chunk, and gaps that empty the machine between bursts.  These
+    are the cases where the re-scoring sweep switches between its walk-free
+    common case and the walk over the group ends."""
+    rng = np.random.default_rng(20261202)
+    for trial in range(24):
+        n = int(rng.choice([70, 130, 400, 1000, 2000]))
+        n_times = int(rng.choice([2, 3, 5, 12]))
+        n_lens = int(rng.choice([1, 2, 4, 9]))
+        gap = int(rng.choice([0, 1, 40]))
+        times = np.cumsum(rng.integers(1, 30, size=n_times)) + gap * np.arange(n_times)
+        lens = rng.integers(1, 60, size=n_lens)
+        inst = 8
+        s = rng.choice(times, size=(inst, n)).astype(np.int32)
+        o = rng.choice(lens, size=(inst, n)).astype(np.int32)
+        p = np.zeros((inst, n), np.int32)
+        a = np.zeros((inst, n), np.int32)
+        kw = dict(B=int(rng.choice([0, 64, 1000])), alpha=int(rng.choice([0, 7, 50, ALPHA_INF])),
+                  M_kv=int(rng.choice([0, 5000])), cost_c=int(rng.integers(0, 9)),
+                  cost_tau=int(rng.integers(0, 4)))
+        ctx = f"start groups trial={trial} n={n} times={n_times} lens={n_lens} gap={gap} {kw}"
+        log(ctx)
+        ref, rv = oracle.decompose(a, p, o, s, **kw)
+        got, gv = gpu_dec(dev, a, p, o, s, **kw)
+        same(ctx, got, ref, gv, rv)
