@@ -167,7 +167,9 @@ struct SimState {
 // its footprint in the batch cost is prompt + progress; fairness stays on
 // progress.  The sweeps are off (completions are taken one event at a time).
 // FILL: with the fill sweep (below), for up to 2 slots per lane.
-template <int POL, int K, int NW, bool GEN, bool ROB, bool PRE, bool FILL>
+// QH: ISJL with up to 2 slots per lane whose plan-queue links are in HBM
+// scratch (else in LDS).
+template <int POL, int K, int NW, bool GEN, bool ROB, bool PRE, bool FILL, bool QH = false>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : (K <= 8 ? 3 : 1)))) void simulate_kernel(SimArgs a) {
   static_assert(!ROB || POL == POL_ISJL, "predicted sizes: ISJL only");
   static_assert(!FILL || (K <= 2 && !ROB && !PRE && POL != POL_LJF), "fill sweep variants");
@@ -182,16 +184,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
   uint16_t* QN = (uint16_t*)(W + a.off_q);
   // ISJL with up to 2 slots per lane: the plan-queue links live in HBM scratch
   // when that lets more waves share a CU (agent-scope accesses, so one lane's
-  // link is seen by the others), else in LDS
-  constexpr bool QGLOBAL = POL == POL_ISJL && K <= 2;
-  uint32_t* QG = (QGLOBAL && a.qlink) ? a.qlink + inst * (int64_t)a.q_stride : nullptr;
+  // link is seen by the others), else in LDS; the launch picks the kernel for
+  // the place (a branch on it at every link would cost the event loop more)
+  constexpr bool QGLOBAL = POL == POL_ISJL && K <= 2 && QH;
+  uint32_t* QG = QGLOBAL ? a.qlink + inst * (int64_t)a.q_stride : nullptr;
   auto qn_set = [&](int r, uint32_t v) {
-    if (QGLOBAL && QG) __hip_atomic_store(QG + r, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if constexpr (QGLOBAL) __hip_atomic_store(QG + r, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     else QN[r] = (uint16_t)v;
   };
   auto qn_get = [&](int r) -> uint32_t {
-    if (QGLOBAL && QG) return __hip_atomic_load(QG + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return QN[r];
+    if constexpr (QGLOBAL) return __hip_atomic_load(QG + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else return QN[r];
   };
   uint16_t* STG = (uint16_t*)(W + a.off_stage);
   // Released ranks on their way into the bitmap (not FCFS); shares the gather
@@ -934,6 +937,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
                 continue;
               }
               // append r to worker wsel's queue
+              wsel = uni(wsel);  // the same in every lane (kept in a scalar register)
               int qt = (int)QNONE;
 #pragma unroll
               for (int k = 0; k < K; ++k)
@@ -978,7 +982,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
             }
             wave_lds_sync();
             // HBM links: every store is done before a plan start reads them
-            if (QGLOBAL && QG) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            if constexpr (QGLOBAL) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
             pmax = wave_max(pmax);
             int idle1 = pmax - alpha;
             if (idle1 < 0) idle1 = 0;
@@ -1982,26 +1986,34 @@ hipError_t launch_sim(const SimArgs& a, int K, int NW, bool general, int wpb, si
   constexpr bool FILL_OK = !ROB && !PRE && POL != POL_LJF;
   constexpr bool FILL_ALWAYS = FILL_OK && POL != POL_ISJL;
   const bool fill = FILL_OK && K <= 2 && (FILL_ALWAYS || a.alpha >= (int)LEN_LIMIT);
-#define FS_LAUNCH(KK, NN, GG, FF)                                                      \
-  if (K == KK && NW == NN && general == GG && fill == FF) {                            \
-    hipLaunchKernelGGL((simulate_kernel<POL, KK, NN, GG, ROB, PRE, FF>), grid, block, lds, s, \
-                       a);                                                             \
-    return hipGetLastError();                                                          \
+  // ISJL plan-queue links in HBM scratch (a kernel of its own, up to 2 slots per
+  // lane; the fill-sweep kernels run with alpha at least every length, so
+  // nothing is planned there)
+  const bool qh = POL == POL_ISJL && K <= 2 && !fill && a.qlink != nullptr;
+#define FS_LAUNCH(KK, NN, GG, FF, QQ)                                                     \
+  if (K == KK && NW == NN && general == GG && fill == FF && qh == QQ) {                   \
+    hipLaunchKernelGGL((simulate_kernel<POL, KK, NN, GG, ROB, PRE, FF, QQ>), grid, block, lds, \
+                       s, a);                                                             \
+    return hipGetLastError();                                                             \
   }
-#define FS_LAUNCH_K(KK, FF)                                                         \
-  FS_LAUNCH(KK, 1, false, FF) FS_LAUNCH(KK, 2, false, FF) FS_LAUNCH(KK, 1, true, FF) \
-  FS_LAUNCH(KK, 2, true, FF)
+#define FS_LAUNCH_K(KK, FF, QQ)                                                             \
+  FS_LAUNCH(KK, 1, false, FF, QQ) FS_LAUNCH(KK, 2, false, FF, QQ) FS_LAUNCH(KK, 1, true, FF, QQ) \
+  FS_LAUNCH(KK, 2, true, FF, QQ)
   if constexpr (FILL_OK) {
-    FS_LAUNCH_K(1, true)
-    FS_LAUNCH_K(2, true)
+    FS_LAUNCH_K(1, true, false)
+    FS_LAUNCH_K(2, true, false)
   }
   if constexpr (!FILL_ALWAYS) {
-    FS_LAUNCH_K(1, false)
-    FS_LAUNCH_K(2, false)
+    FS_LAUNCH_K(1, false, false)
+    FS_LAUNCH_K(2, false, false)
   }
-  FS_LAUNCH_K(4, false)
-  FS_LAUNCH_K(8, false)
-  FS_LAUNCH_K(16, false)
+  if constexpr (POL == POL_ISJL) {
+    FS_LAUNCH_K(1, false, true)
+    FS_LAUNCH_K(2, false, true)
+  }
+  FS_LAUNCH_K(4, false, false)
+  FS_LAUNCH_K(8, false, false)
+  FS_LAUNCH_K(16, false, false)
 #undef FS_LAUNCH_K
 #undef FS_LAUNCH
   return hipErrorInvalidValue;
