@@ -365,6 +365,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
   int ws_plan[K];  // ROB: KV reservation of the running job (from its planning size)
   int ws_p[K];     // PRE: prompt of the running job (its footprint offset)
   uint32_t ws_q[K];
+  uint32_t ws_qn[K];  // links in HBM: the link of the queue's head, loaded ahead
   bool valid[K];
 #pragma unroll
   for (int k = 0; k < K; ++k) {
@@ -373,6 +374,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
     ws_start[k] = IDLE;
     ws_end[k] = IDLE;
     ws_q[k] = QNONE | (QNONE << 16);
+    ws_qn[k] = QNONE;
     valid[k] = (k * WAVE + lane) < Beff;
   }
   PoolBits<NW> pool;
@@ -982,7 +984,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
             }
             wave_lds_sync();
             // HBM links: every store is done before a plan start reads them
-            if constexpr (QGLOBAL) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            if constexpr (QGLOBAL) {
+              __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+              // each head's link, loaded now for when it starts
+#pragma unroll
+              for (int k = 0; k < K; ++k) {
+                const uint32_t h = ws_q[k] & 0xFFFFu;
+                ws_qn[k] = h != QNONE ? qn_get((int)h) : QNONE;
+              }
+            }
             pmax = wave_max(pmax);
             int idle1 = pmax - alpha;
             if (idle1 < 0) idle1 = 0;
@@ -1060,7 +1070,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
               }
               mlen = min(mlen, len);
               emit(pid(wv), t, len);
-              uint32_t nx = qn_get((int)h);
+              uint32_t nx;
+              if constexpr (QGLOBAL) {  // loaded ahead; the new head's link is loaded now
+                nx = ws_qn[k];
+                ws_qn[k] = nx != QNONE ? qn_get((int)nx) : QNONE;
+              } else {
+                nx = qn_get((int)h);
+              }
               ws_q[k] = (nx == QNONE) ? (QNONE | (QNONE << 16)) : (nx | (ws_q[k] & 0xFFFF0000u));
             }
           }
