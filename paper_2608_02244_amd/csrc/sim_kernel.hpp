@@ -170,7 +170,7 @@ struct SimState {
 // QH: ISJL with up to 2 slots per lane whose plan-queue links are in HBM
 // scratch (else in LDS).
 template <int POL, int K, int NW, bool GEN, bool ROB, bool PRE, bool FILL, bool QH = false>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : (K <= 8 ? 3 : 1)))) void simulate_kernel(SimArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <= 2 ? 4 : (K <= 8 ? 3 : 1)))) void simulate_kernel(SimArgs a) {
   static_assert(!ROB || POL == POL_ISJL, "predicted sizes: ISJL only");
   static_assert(!FILL || (K <= 2 && !ROB && !PRE && POL != POL_LJF), "fill sweep variants");
   extern __shared__ uint32_t lds_raw[];
@@ -420,6 +420,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
   int64_t acc_E = 0, acc_SM = 0, acc_SSM = 0, acc_ext = 0, acc_busy = 0, acc_peak = 0,
           acc_unfair = 0;
   int acc_maxext = 0, acc_maxact = 0;
+  // With up to 2 slots per lane the sweeps' per-lane partial sums (and the
+  // largest footprint) of their span terms carry over from sweep to sweep and
+  // are summed over the wave once after the event loop: integer sums, so the
+  // deferral changes no result, and a sweep ends without a reduction.  The
+  // wider kernels have no registers to spare for them and reduce per sweep.
+  constexpr bool DEFER = K <= 2;
+  int64_t pE = 0, pSM = 0, pSSM = 0, pX = 0, pP = 0;
+  int pU = 0;
   int32_t* st_out = a.start ? a.start + row : nullptr;
   int32_t* fi_out = a.finish ? a.finish + row : nullptr;
   const int iter_max = 8 * n + 64;
@@ -1218,7 +1226,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
           int de[K];  // completion - t of each position (IDLE past N)
 #pragma unroll
           for (int k = 0; k < K; ++k) de[k] = lane * K + k < N ? (int)dk[k] : IDLE;
-          const int e_up = __shfl_down(de[0], 1);  // first position of the next lane
+          const int e_up = dpp<DPP_WAVE_SHL1>(de[0], de[0]);  // first position of the next lane
           // progress sum / max / min of the positions of the lanes above
           int xs_g, xs_max, xs_min;
           {
@@ -1409,8 +1417,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
           const int A_m = p_m >= 0 ? at_pos_u(ap, p_m) : 0;
           // spans after each counted event, with the jobs at the positions
           // above and the admitted jobs 0..A-1
-          int64_t lE = 0, lSM = 0, lSSM = 0, lX = 0, lP = 0;
-          int lU = 0, lmx = 0, lma = 0;
+          int64_t qE = 0, qSM = 0, qSSM = 0, qX = 0, qP = 0;
+          int qU = 0;
+          int64_t &lE = DEFER ? pE : qE, &lSM = DEFER ? pSM : qSM, &lSSM = DEFER ? pSSM : qSSM,
+                  &lX = DEFER ? pX : qX, &lP = DEFER ? pP : qP;
+          int& lU = DEFER ? pU : qU;
+          int lmx = 0, lma = 0;
           {
             int cg = xs_g, cg_max = xs_max, cg_min = xs_min;
 #pragma unroll
@@ -1452,27 +1464,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
             const int64_t D = (int64_t)(p_m >= 0 ? e_first : tau_rel), s = N;
             const int64_t m0 = (int64_t)(t - S.min_s) + 1;
             const int64_t sm = D * m0 + D * (D - 1) / 2;
-            if (lane == 0) {
-              lE += D * (S.sum_s - s * (int64_t)S.min_s);
-              lSM += sm;
-              lSSM += s * sm;
-              const int ext = S.max_s - S.min_s;
-              lX += D * ext;
-              if (ext > alpha) lU += (int)D;
-              lP = max(lP, s * (int64_t)(t + D) - S.sum_s);
-              lmx = max(lmx, ext);
-              lma = max(lma, N);
-            }
+            acc_E += D * (S.sum_s - s * (int64_t)S.min_s);
+            acc_SM += sm;
+            acc_SSM += s * sm;
+            const int ext = S.max_s - S.min_s;
+            acc_ext += D * ext;
+            if (ext > alpha) acc_unfair += D;
+            acc_peak = max(acc_peak, s * (int64_t)(t + D) - S.sum_s);
+            lmx = max(lmx, ext);
+            lma = max(lma, N);
           }
-          const int64_t span = (int64_t)tau_rel;
-          const int64_t sSM = wave_sum64(lSM), sSSM = wave_sum64(lSSM);
-          acc_E += wave_sum64(lE);
-          acc_SM += sSM;
-          acc_SSM += sSSM;
-          acc_ext += wave_sum64(lX);
-          acc_busy += span;
-          acc_unfair += wave_sum(lU);
-          acc_peak = max(acc_peak, wave_max64(lP));
+          if constexpr (!DEFER) {
+            acc_E += wave_sum64(lE);
+            acc_SM += wave_sum64(lSM);
+            acc_SSM += wave_sum64(lSSM);
+            acc_ext += wave_sum64(lX);
+            acc_unfair += wave_sum(lU);
+            acc_peak = max(acc_peak, wave_max64(lP));
+          }
+          acc_busy += (int64_t)tau_rel;
           acc_maxext = max(acc_maxext, wave_max(lmx));
           acc_maxact = max(acc_maxact, wave_max(lma));
           // completions of the admitted jobs
@@ -1628,8 +1638,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
       const int gbits = 32 - __builtin_clz((uint32_t)(t - S.min_s) | 1u);
       const bool packed = gbits < 32 && (int64_t)maxlen < (int64_t)(0xFFFFFFFFu >> gbits);
       int stop = 0, e0 = 0, st_g = 0, st_gmax = -1, st_gmin = IDLE, tau_end = 0;
-      int64_t lE = 0, lSM = 0, lSSM = 0, lX = 0, lP = 0;
-      int lU = 0;
+      int64_t qE = 0, qSM = 0, qSSM = 0, qX = 0, qP = 0;
+      int qU = 0;
+      int64_t &lE = DEFER ? pE : qE, &lSM = DEFER ? pSM : qSM, &lSSM = DEFER ? pSSM : qSSM,
+              &lX = DEFER ? pX : qX, &lP = DEFER ? pP : qP;
+      int& lU = DEFER ? pU : qU;
       // Sort the N completions into KS registers per lane (position
       // p = lane * KS + k holds the p-th) and account the spans.  KS = K sorts
       // every slot in place; KS = 1 first packs up to 64 active slots into one
@@ -1703,7 +1716,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
           }
         }
         // completion time of the first position of the next lane
-        const int e_up = t + (int)(uint32_t)__shfl_down((int)dk[0], 1);
+        const int e_up = t + dpp<DPP_WAVE_SHL1>((int)dk[0], (int)dk[0]);
         // Stop position: the lowest position ending a tie group after which
         // the machine is empty or A_max <= alpha (A_max right after the
         // completions at e is e - t + the largest progress still active).
@@ -1782,27 +1795,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
         const int64_t D = (int64_t)(e0 - t), s = N;
         const int64_t m0 = (int64_t)(t - S.min_s) + 1;
         const int64_t sm = D * m0 + D * (D - 1) / 2;
-        if (lane == 0) {
-          lE += D * (S.sum_s - s * (int64_t)S.min_s);
-          lSM += sm;
-          lSSM += s * sm;
-          const int ext = S.max_s - S.min_s;
-          lX += D * ext;
-          if (ext > alpha) lU += (int)D;
-          lP = max(lP, s * (int64_t)e0 - S.sum_s);
-        }
-        acc_maxext = max(acc_maxext, S.max_s - S.min_s);
+        acc_E += D * (S.sum_s - s * (int64_t)S.min_s);
+        acc_SM += sm;
+        acc_SSM += s * sm;
+        const int ext = S.max_s - S.min_s;
+        acc_ext += D * ext;
+        if (ext > alpha) acc_unfair += D;
+        acc_peak = max(acc_peak, s * (int64_t)e0 - S.sum_s);
+        acc_maxext = max(acc_maxext, ext);
         acc_maxact = max(acc_maxact, N);
       }
-      const int64_t span = (int64_t)(tau_end - t);
-      const int64_t sSM = wave_sum64(lSM), sSSM = wave_sum64(lSSM);
-      acc_E += wave_sum64(lE);
-      acc_SM += sSM;
-      acc_SSM += sSSM;
-      acc_ext += wave_sum64(lX);
-      acc_busy += span;
-      acc_unfair += wave_sum(lU);
-      acc_peak = max(acc_peak, wave_max64(lP));
+      if constexpr (!DEFER) {
+        acc_E += wave_sum64(lE);
+        acc_SM += wave_sum64(lSM);
+        acc_SSM += wave_sum64(lSSM);
+        acc_ext += wave_sum64(lX);
+        acc_unfair += wave_sum(lU);
+        acc_peak = max(acc_peak, wave_max64(lP));
+      }
+      acc_busy += (int64_t)(tau_end - t);
       if (POL == POL_ISJL && amax_sweep && mode == 0) {
         // Phase TWO switches to DRAIN at the first event before tau_end with an
         // idle worker that has nothing planned (from its first completion, or
@@ -1962,6 +1973,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL ? 4 : 
       acc_peak = max(acc_peak, s * (int64_t)tn - S.sum_s + (PRE ? S.sp : 0));
     }
     S.t = tn;
+  }
+  if constexpr (DEFER) {
+    acc_E += wave_sum64(pE);
+    acc_SM += wave_sum64(pSM);
+    acc_SSM += wave_sum64(pSSM);
+    acc_ext += wave_sum64(pX);
+    acc_unfair += wave_sum(pU);
+    acc_peak = max(acc_peak, wave_max64(pP));
   }
 
   if (failed) {
