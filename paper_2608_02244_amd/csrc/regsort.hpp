@@ -121,49 +121,25 @@ __device__ __forceinline__ void half_lanes(uint32_t (&key)[KS], int lane) {
 }
 
 // Sort the 64 * KS keys held in registers, ascending in lane-major order.
-template <int KS, bool MED3 = false>
-__device__ inline void reg_sort_keys(uint32_t (&key)[KS], int lane) {
-  for (int size = 2; size <= KS * WAVE; size <<= 1) {
-    if (size <= KS) {
-      switch (size) {
-        case 2: if constexpr (KS >= 2) lm_mirror_regs<2>(key); break;
-        case 4: if constexpr (KS >= 4) lm_mirror_regs<4>(key); break;
-        case 8: if constexpr (KS >= 8) lm_mirror_regs<8>(key); break;
-        case 16: if constexpr (KS >= 16) lm_mirror_regs<16>(key); break;
-        case 32: if constexpr (KS >= 32) lm_mirror_regs<32>(key); break;
-        default: if constexpr (KS >= 64) lm_mirror_regs<64>(key); break;
-      }
-    } else {
-      switch (size / KS) {
-        case 2: mirror_lanes<1, KS, MED3>(key, lane); break;
-        case 4: mirror_lanes<3, KS, MED3>(key, lane); break;
-        case 8: mirror_lanes<7, KS, MED3>(key, lane); break;
-        case 16: mirror_lanes<15, KS, MED3>(key, lane); break;
-        case 32: mirror_lanes<31, KS, MED3>(key, lane); break;
-        default: mirror_lanes<63, KS, MED3>(key, lane); break;
-      }
-    }
-    for (int d = size >> 2; d > 0; d >>= 1) {
-      if (d < KS) {
-        switch (d) {
-          case 1: if constexpr (KS > 1) lm_half_regs<1>(key); break;
-          case 2: if constexpr (KS > 2) lm_half_regs<2>(key); break;
-          case 4: if constexpr (KS > 4) lm_half_regs<4>(key); break;
-          case 8: if constexpr (KS > 8) lm_half_regs<8>(key); break;
-          case 16: if constexpr (KS > 16) lm_half_regs<16>(key); break;
-          default: if constexpr (KS > 32) lm_half_regs<32>(key); break;
-        }
-      } else {
-        switch (d / KS) {
-          case 1: half_lanes<1, KS, MED3>(key, lane); break;
-          case 2: half_lanes<2, KS, MED3>(key, lane); break;
-          case 4: half_lanes<4, KS, MED3>(key, lane); break;
-          case 8: half_lanes<8, KS, MED3>(key, lane); break;
-          case 16: half_lanes<16, KS, MED3>(key, lane); break;
-          default: half_lanes<32, KS, MED3>(key, lane); break;
-        }
-      }
-    }
+// The stages are expanded at compile time (merge sizes 2, 4, .. 64 * KS, each
+// a mirror step and half-cleaners of distance size/4 .. 1), so every stage is
+// straight-line code with its exchange pattern fixed.
+template <int KS, bool MED3, int D>
+__device__ __forceinline__ void reg_sort_halves(uint32_t (&key)[KS], int lane) {
+  if constexpr (D > 0) {
+    if constexpr (D < KS) lm_half_regs<D>(key);
+    else half_lanes<D / KS, KS, MED3>(key, lane);
+    reg_sort_halves<KS, MED3, D / 2>(key, lane);
+  }
+}
+
+template <int KS, bool MED3 = false, int SIZE = 2>
+__device__ __forceinline__ void reg_sort_keys(uint32_t (&key)[KS], int lane) {
+  if constexpr (SIZE <= KS * WAVE) {
+    if constexpr (SIZE <= KS) lm_mirror_regs<SIZE>(key);
+    else mirror_lanes<SIZE / KS - 1, KS, MED3>(key, lane);
+    reg_sort_halves<KS, MED3, SIZE / 4>(key, lane);
+    reg_sort_keys<KS, MED3, SIZE * 2>(key, lane);
   }
 }
 
@@ -203,28 +179,23 @@ __device__ __forceinline__ void lmp_cx_lanes(uint32_t (&key)[KS], int (&val)[KS]
   }
 }
 
-template <int KS>
-__device__ inline void reg_sort_payload(uint32_t (&key)[KS], int (&val)[KS], int lane) {
-  for (int size = 2; size <= KS * WAVE; size <<= 1) {
-    for (int d = size >> 1; d > 0; d >>= 1) {
-      if (d < KS) {
-        switch (d) {
-          case 1: if constexpr (KS > 1) lmp_cx_regs<1>(key, val, size, lane); break;
-          case 2: if constexpr (KS > 2) lmp_cx_regs<2>(key, val, size, lane); break;
-          case 4: if constexpr (KS > 4) lmp_cx_regs<4>(key, val, size, lane); break;
-          default: if constexpr (KS > 8) lmp_cx_regs<8>(key, val, size, lane); break;
-        }
-      } else {
-        switch (d / KS) {
-          case 1: lmp_cx_lanes<1>(key, val, size, lane); break;
-          case 2: lmp_cx_lanes<2>(key, val, size, lane); break;
-          case 4: lmp_cx_lanes<4>(key, val, size, lane); break;
-          case 8: lmp_cx_lanes<8>(key, val, size, lane); break;
-          case 16: lmp_cx_lanes<16>(key, val, size, lane); break;
-          default: lmp_cx_lanes<32>(key, val, size, lane); break;
-        }
-      }
-    }
+template <int KS, int SIZE, int D>
+__device__ __forceinline__ void reg_sort_payload_stage(uint32_t (&key)[KS], int (&val)[KS],
+                                                       int lane) {
+  if constexpr (D > 0) {
+    if constexpr (D < KS) lmp_cx_regs<D>(key, val, SIZE, lane);
+    else lmp_cx_lanes<D / KS>(key, val, SIZE, lane);
+    reg_sort_payload_stage<KS, SIZE, D / 2>(key, val, lane);
+  }
+}
+
+// Merge sizes 2, 4, .. 64 * KS, each with exchanges of distance size/2 .. 1,
+// expanded at compile time like the keys-only sort.
+template <int KS, int SIZE = 2>
+__device__ __forceinline__ void reg_sort_payload(uint32_t (&key)[KS], int (&val)[KS], int lane) {
+  if constexpr (SIZE <= KS * WAVE) {
+    reg_sort_payload_stage<KS, SIZE, SIZE / 2>(key, val, lane);
+    reg_sort_payload<KS, SIZE * 2>(key, val, lane);
   }
 }
 
