@@ -560,6 +560,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
       }
       tot64 = run - S.res;
     }
+    // the count in a scalar register, so the walk over the slot registers
+    // below branches on it rather than masking lanes (measured on the kernels
+    // with more than 2 slots per lane; the narrower ones ran no faster)
+    if constexpr (K > 2) na = uni(na);
     if (na == 0) return 0;
     int base = 0, lsum = 0, lplan = 0, lmin = IDLE, lp = 0, lpmax = -IDLE;
 #pragma unroll
