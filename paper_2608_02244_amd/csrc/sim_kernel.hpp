@@ -225,6 +225,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
   const int NP = a.NP;
   int bad = 0, big = 0, unsorted = 0, maxlen = 0, maxfoot = 0, maxarr = 0;
   int64_t osum = 0, qsum = 0, rsum = 0;
+  uint64_t q2 = 0;  // twice the footprint sum Q: one 32 x 32 -> 64 product per job
   int carry_ar = 0;
   // The rows are software-pipelined: the loads of row r + PF are issued
   // while row r is processed, so PF rows of loads are in flight (clamped
@@ -272,8 +273,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
       if (foot < LEN_LIMIT && foot > maxfoot) maxfoot = (int)foot;
       if (ar > maxarr) maxarr = ar;
       osum += (int64_t)p + (int64_t)o;  // tokens served
-      // Q: the footprint summed over the job's own steps (Section 5)
-      qsum += PRE ? (int64_t)o * p + (int64_t)o * (o + 1) / 2 : len * (len + 1) / 2;
+      // Q: the footprint summed over the job's own steps (Section 5), doubled:
+      // len (len + 1), or o (2 p + o + 1) with the prompt prefilled; both
+      // factors are below 2^22 in every instance that is simulated (a larger
+      // footprint returns the too-large marker before Q is used)
+      q2 += PRE ? (uint64_t)(uint32_t)o * (uint32_t)(2 * p + o + 1)
+                : (uint64_t)(uint32_t)len * (uint32_t)(len + 1);
       rsum += ar;
       const uint32_t l32 = (uint32_t)(ROB ? plan_len : len) & LMASK;
       if (POL == POL_LJF || POL == POL_ISJL) key = ((LMASK - l32) << 12) | (uint32_t)i;
@@ -303,7 +308,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
   maxfoot = wave_max(maxfoot);
   maxarr = wave_max(maxarr);
   osum = wave_sum64(osum);
-  qsum = wave_sum64(qsum);
+  qsum = (int64_t)((uint64_t)wave_sum64((int64_t)q2) >> 1);  // every term is even
   rsum = wave_sum64(rsum);
   if (GEN && maxarr >= ARR_LIMIT) {
     write_marker(a.out, a.out_T, inst, FSCHED_T_TOOLARGE, lane);
@@ -330,12 +335,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
   if (!(POL == POL_FCFS && !GEN)) {
     wave_lds_sync();
     switch (NP) {
-      case 64: wave_reg_sort<1>(W, lane); break;
-      case 128: wave_reg_sort<2>(W, lane); break;
-      case 256: wave_reg_sort<4>(W, lane); break;
-      case 512: wave_reg_sort<8>(W, lane); break;
-      case 1024: wave_reg_sort<16>(W, lane); break;
-      case 2048: wave_reg_sort<32>(W, lane); break;
+      case 64: wave_reg_sort<1, true>(W, lane); break;
+      case 128: wave_reg_sort<2, true>(W, lane); break;
+      case 256: wave_reg_sort<4, true>(W, lane); break;
+      case 512: wave_reg_sort<8, true>(W, lane); break;
+      case 1024: wave_reg_sort<16, true>(W, lane); break;
+      case 2048: wave_reg_sort<32, true>(W, lane); break;
       default: wave_bitonic_sort(W, NP, lane); break;
     }
     wave_lds_sync();
