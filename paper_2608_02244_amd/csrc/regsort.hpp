@@ -82,9 +82,9 @@ __device__ __forceinline__ void lm_half_lanes(uint32_t (&key)[KS], int lane) {
 // median of three: with c = 0 it is min(a, b) and with c = ~0u max(a, b), c
 // chosen per lane.  One instruction fewer per key, but a DPP partner then
 // needs a register of its own instead of fusing into the min and the max:
-// taken by the re-scoring kernel and by the simulation kernels' priority sort
-// (before their event loop), not by the sweeps' sorts inside the event loop,
-// where the registers are at their limit.
+// taken by the re-scoring kernel and by the simulation kernels' priority and
+// drain-sweep sorts (measured faster there; the payload sorts keep the
+// min / max form).
 __device__ __forceinline__ uint32_t umed3(uint32_t a, uint32_t b, uint32_t c) {
   return max(min(a, b), min(max(a, b), c));
 }

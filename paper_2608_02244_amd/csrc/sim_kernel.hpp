@@ -1683,7 +1683,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
             dk[0] = lane < N ? PEND[lane] : 0xFFFFFFFFu;
             wave_lds_sync();
           }
-          reg_sort_keys<KS>(dk, lane);
+          reg_sort_keys<KS, true>(dk, lane);
           const uint32_t gmask = (1u << gbits) - 1u;
 #pragma unroll
           for (int k = 0; k < KS; ++k) {
