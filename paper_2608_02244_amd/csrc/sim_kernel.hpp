@@ -875,6 +875,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
                 if (fm) m = min(Bp, k * WAVE + __builtin_ctzll(fm));
               }
             }
+            if constexpr (K <= 4) m = uni(m);  // scalar (measured: the 8-slot kernel ran slower)
             const int beta = a.beta;
             int cap[K], load[K];
 #pragma unroll
@@ -898,7 +899,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
             // each goes to the first spare worker with room, else to the long
             // worker of largest index with room; a job that fits nowhere stays.
             int cur = rlast;
-            const bool has_spare = Bp > m;
+            const bool has_spare = uni(Bp) > m;
+            // Each worker choice below is one ballot per slot register, built
+            // from plain comparisons (no short-circuit, which the compiler
+            // turns into lane-masked branches and leaves the worker index in a
+            // vector register).  With up to 4 slots per lane the spare and long
+            // workers' lane masks are kept; the wider kernels, short of scalar
+            // registers, test the ranges in the ballot itself.
+            uint64_t spare_m[K], long_m[K];
+            if constexpr (K <= 4) {
+#pragma unroll
+              for (int k = 0; k < K; ++k) {
+                const int w = k * WAVE + lane;
+                spare_m[k] = ballot((w >= m) & (w < Bp));
+                long_m[k] = ballot((w >= 1) & (w < m));
+              }
+            }
             while (true) {
               const int r = pool.first_from(cur + 1, lane);
               if (r < 0) break;
@@ -908,7 +924,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
 #pragma unroll
                 for (int k = 0; k < K; ++k) {
                   const int w = k * WAVE + lane;
-                  const uint64_t ms = ballot(w >= m && w < Bp && cap[k] - load[k] >= len);
+                  const uint64_t ms = K <= 4 ? ballot(cap[k] - load[k] >= len) & spare_m[k]
+                                             : ballot((w >= m) & (w < Bp) & (cap[k] - load[k] >= len));
                   if (ms) {
                     wsel = k * WAVE + __builtin_ctzll(ms);
                     break;
@@ -919,7 +936,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
 #pragma unroll
                 for (int k = K - 1; k >= 0; --k) {
                   const int w = k * WAVE + lane;
-                  const uint64_t ml = ballot(w >= 1 && w < m && cap[k] - load[k] >= len);
+                  const uint64_t ml = K <= 4 ? ballot(cap[k] - load[k] >= len) & long_m[k]
+                                             : ballot((w >= 1) & (w < m) & (cap[k] - load[k] >= len));
                   if (ml) {
                     wsel = k * WAVE + 63 - __builtin_clzll(ml);
                     break;
