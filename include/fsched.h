@@ -248,7 +248,7 @@ int fsched_bruteforce_opt(const fsched_params* p, int64_t n_inst, int32_t n_jobs
  * serving loops, harnesses that forbid hipMalloc.  It allocates nothing: no
  * hipMalloc / hipFree / pool allocation and no host staging.  Its scratch (the
  * rank table of 2 bytes per job, rows rounded up to 64 jobs, for every policy
- * but FCFS; for ISJL with at most 128 workers and a finite alpha, when the
+ * but FCFS; for ISJL with at most 512 workers and a finite alpha, when the
  * plan-queue links do not fit LDS, 4 bytes per job rounded up to a power of two
  * (at least 64)) is a fixed buffer of FSCHED_NOALLOC_SCRATCH_BYTES per device,
  * part of the library's image and held by each device the library runs on
@@ -259,7 +259,8 @@ int fsched_bruteforce_opt(const fsched_params* p, int64_t n_inst, int32_t n_jobs
  *     fsched_simulate.  FSCHED_F_SYNC synchronises the stream before return.
  *   - A call whose scratch would exceed FSCHED_NOALLOC_SCRATCH_BYTES returns
  *     FSCHED_ESCRATCH before enqueuing anything (e.g. at 2,000 jobs per
- *     instance and B = 512: 16,384 instances fit 64 MiB).
+ *     instance, B = 512 and a finite alpha, 12 KiB per instance: 5,461
+ *     instances fit 64 MiB).
  *   - Every call on one device shares that device's buffer: calls that overlap
  *     in time on one device (on different streams, or from several threads)
  *     race and give undefined results.  Calls in order on one stream are safe.

@@ -143,11 +143,11 @@ int simulate_layout(const fsched_params* p, int64_t n_inst, int32_t n, SimLayout
   const bool isjl = p->policy == FSCHED_ISJL;
   // plan-queue links; with alpha = infinity Phase ONE never plans (no second
   // job is longer than alpha), so the links are not needed
-  // (with up to 2 slots per lane, at most 128 VGPRs, 16 waves fit a CU: the
+  // (with up to 8 slots per lane, at most 128 VGPRs, 16 waves fit a CU: the
   // links go to HBM scratch when in LDS they would cap a CU below that)
   const bool plans = isjl && p->alpha != FSCHED_ALPHA_INF;
   bool q_hbm = false;
-  if (plans && K <= 2) {
+  if (plans && K <= 8) {
     const int w_lds = NP + NP / 2 +
                       std::max((Beff + 1) / 2, 64 * NW);  // words per wave with the links
     const size_t per_wave = (size_t)((w_lds + 3) & ~3) * 4;

@@ -167,14 +167,21 @@ struct SimState {
 // its footprint in the batch cost is prompt + progress; fairness stays on
 // progress.  The sweeps are off (completions are taken one event at a time).
 // FILL: with the fill sweep (below), for up to 2 slots per lane.
-// QH: ISJL with up to 2 slots per lane whose plan-queue links are in HBM
-// scratch (else in LDS).
+// QH: ISJL with up to 8 slots per lane whose plan-queue links are in HBM
+// scratch (else in LDS).  With 4 or 8 slots per lane such a kernel is also held
+// to 128 VGPRs, so that with the LDS the links free 16 waves share a CU.
 template <int POL, int K, int NW, bool GEN, bool ROB, bool PRE, bool FILL, bool QH = false>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <= 2 ? 4 : (K <= 8 ? 3 : 1)))) void simulate_kernel(SimArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <= 2 || (QH && K <= 8) ? 4 : (K <= 8 ? 3 : 1)))) void simulate_kernel(SimArgs a) {
   static_assert(!ROB || POL == POL_ISJL, "predicted sizes: ISJL only");
   static_assert(!FILL || (K <= 2 && !ROB && !PRE && POL != POL_LJF), "fill sweep variants");
   extern __shared__ uint32_t lds_raw[];
-  const int wib = threadIdx.x >> 6;
+  // With 4 or 8 slots per lane and the links in HBM the wave's index in its
+  // block is taken into a scalar register: every row pointer derived from the
+  // instance is then scalar, which is what brings those kernels under 128
+  // VGPRs (the narrower kernels ran slower with it, their scalar registers
+  // being the scarcer ones).
+  const int wib = (QH && K >= 4) ? __builtin_amdgcn_readfirstlane(threadIdx.x >> 6)
+                                 : (int)(threadIdx.x >> 6);
   const int64_t inst = (int64_t)blockIdx.x * (blockDim.x >> 6) + wib;
   if (inst >= a.n_inst) return;
   const int lane = lane_id();
@@ -182,11 +189,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
   uint32_t* W = lds_raw + (size_t)wib * (size_t)a.wave_words;
   int32_t* ARR = (int32_t*)(W + a.off_arr);
   uint16_t* QN = (uint16_t*)(W + a.off_q);
-  // ISJL with up to 2 slots per lane: the plan-queue links live in HBM scratch
+  // ISJL with up to 8 slots per lane: the plan-queue links live in HBM scratch
   // when that lets more waves share a CU (agent-scope accesses, so one lane's
   // link is seen by the others), else in LDS; the launch picks the kernel for
   // the place (a branch on it at every link would cost the event loop more)
-  constexpr bool QGLOBAL = POL == POL_ISJL && K <= 2 && QH;
+  constexpr bool QGLOBAL = POL == POL_ISJL && K <= 8 && QH;
   uint32_t* QG = QGLOBAL ? a.qlink + inst * (int64_t)a.q_stride : nullptr;
   auto qn_set = [&](int r, uint32_t v) {
     if constexpr (QGLOBAL) __hip_atomic_store(QG + r, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -2048,10 +2055,10 @@ hipError_t launch_sim(const SimArgs& a, int K, int NW, bool general, int wpb, si
   constexpr bool FILL_OK = !ROB && !PRE && POL != POL_LJF;
   constexpr bool FILL_ALWAYS = FILL_OK && POL != POL_ISJL;
   const bool fill = FILL_OK && K <= 2 && (FILL_ALWAYS || a.alpha >= (int)LEN_LIMIT);
-  // ISJL plan-queue links in HBM scratch (a kernel of its own, up to 2 slots per
+  // ISJL plan-queue links in HBM scratch (a kernel of its own, up to 8 slots per
   // lane; the fill-sweep kernels run with alpha at least every length, so
   // nothing is planned there)
-  const bool qh = POL == POL_ISJL && K <= 2 && !fill && a.qlink != nullptr;
+  const bool qh = POL == POL_ISJL && K <= 8 && !fill && a.qlink != nullptr;
 #define FS_LAUNCH(KK, NN, GG, FF, QQ)                                                     \
   if (K == KK && NW == NN && general == GG && fill == FF && qh == QQ) {                   \
     hipLaunchKernelGGL((simulate_kernel<POL, KK, NN, GG, ROB, PRE, FF, QQ>), grid, block, lds, \
@@ -2072,6 +2079,8 @@ hipError_t launch_sim(const SimArgs& a, int K, int NW, bool general, int wpb, si
   if constexpr (POL == POL_ISJL) {
     FS_LAUNCH_K(1, false, true)
     FS_LAUNCH_K(2, false, true)
+    FS_LAUNCH_K(4, false, true)
+    FS_LAUNCH_K(8, false, true)
   }
   FS_LAUNCH_K(4, false, false)
   FS_LAUNCH_K(8, false, false)

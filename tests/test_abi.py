@@ -105,5 +105,8 @@ def test_noalloc_argument_errors_before_device_work():
     assert call_noalloc(p, n_jobs=4097) == fs.ETOOLARGE
     # 65,536 x 2,000 jobs: a 256 MiB rank table against the 64 MiB buffer
     assert call_noalloc(p, n_inst=65536, n_jobs=2000) == fs.ESCRATCH
+    # 8 slots per lane at a finite alpha: the plan links in HBM add 8 KiB to the
+    # 4 KiB rank row, so 5,462 instances of 2,000 jobs no longer fit
+    assert call_noalloc(p, n_inst=5462, n_jobs=2000) == fs.ESCRATCH
     assert call_noalloc(fs.make_params("fcfs", 512, 128, device=True), n_inst=65536,
                         n_jobs=2000, ptr=None) == fs.EINVAL

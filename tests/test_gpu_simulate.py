@@ -438,11 +438,13 @@ def test_rank_scratch_reuse_across_calls_and_streams(dev):
 
 @pytest.mark.parametrize("alpha", [2, 40, 300])
 def test_plan_links_in_hbm(dev, alpha):
-    """ISJL with up to 2 slots per lane and 2,000 jobs: the plan-queue links would
+    """ISJL with up to 8 slots per lane and 2,000 jobs: the plan-queue links would
     cap a CU below 16 waves in LDS, so they go to HBM scratch (also for the
-    predicted-size and prefill variants)."""
+    predicted-size and prefill variants); 4 and 8 slots per lane also take the
+    kernels held to 128 VGPRs."""
     rng = np.random.default_rng(zlib.crc32(f"qlinks:{alpha}".encode()))
-    for B, M, arr in ((100, 0, 0), (128, 12000, 4000), (70, 6000, -3000)):
+    for B, M, arr in ((100, 0, 0), (128, 12000, 4000), (70, 6000, -3000), (200, 30000, 3000),
+                      (512, 0, 0), (400, 45000, -3000)):
         a, p, o = workload.random_tables(rng, 5, 2000, 60, 200, max_arrival=abs(arr),
                                          sorted_arrivals=arr > 0)
         kw = dict(B=B, alpha=alpha, M_kv=M, cost_c=3, cost_tau=1)

@@ -52,9 +52,11 @@ def test_noalloc_equals_simulate_two_calls(dev):
     # scratch (rank table and plan-queue links); second: fewer, shorter instances
     log("noalloc call 1: bimodal_sweep 512 instances, ISJL alpha=256")
     both(dev, "bimodal_sweep_4096x2000", 512, policy="isjl", alpha=256)
-    log("noalloc call 2: lognormal 96 instances, ISJL alpha=64")
+    log("noalloc call 2: pareto 192 instances, ISJL alpha=128 (8 slots per lane)")
+    both(dev, "pareto_65536x2000", 192, policy="isjl", alpha=128)
+    log("noalloc call 3: lognormal 96 instances, ISJL alpha=64")
     both(dev, "lognormal_4096x1000", 96, policy="isjl", alpha=64)
-    log("noalloc call 3: lognormal 40 instances, SJF")
+    log("noalloc call 4: lognormal 40 instances, SJF")
     both(dev, "lognormal_4096x1000", 40, policy="sjf", alpha=fs.ALPHA_INF)
 
 
