@@ -168,20 +168,22 @@ struct SimState {
 // progress.  The sweeps are off (completions are taken one event at a time).
 // FILL: with the fill sweep (below), for up to 2 slots per lane.
 // QH: ISJL with up to 8 slots per lane whose plan-queue links are in HBM
-// scratch (else in LDS).  With 4 or 8 slots per lane such a kernel is also held
-// to 128 VGPRs, so that with the LDS the links free 16 waves share a CU.
+// scratch (else in LDS).  Every kernel with up to 8 slots per lane but FCFS's
+// is held to 128 VGPRs, so that 4 waves share a SIMD where the LDS allows 16
+// per CU (FCFS's 4- and 8-slot kernels ran slower that way and keep 3).
 template <int POL, int K, int NW, bool GEN, bool ROB, bool PRE, bool FILL, bool QH = false>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <= 2 || (QH && K <= 8) ? 4 : (K <= 8 ? 3 : 1)))) void simulate_kernel(SimArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <= 2 || (K <= 8 && POL != POL_FCFS) ? 4 : (K <= 8 ? 3 : 1)))) void simulate_kernel(SimArgs a) {
   static_assert(!ROB || POL == POL_ISJL, "predicted sizes: ISJL only");
   static_assert(!FILL || (K <= 2 && !ROB && !PRE && POL != POL_LJF), "fill sweep variants");
   extern __shared__ uint32_t lds_raw[];
-  // With 4 or 8 slots per lane and the links in HBM the wave's index in its
-  // block is taken into a scalar register: every row pointer derived from the
-  // instance is then scalar, which is what brings those kernels under 128
-  // VGPRs (the narrower kernels ran slower with it, their scalar registers
-  // being the scarcer ones).
-  const int wib = (QH && K >= 4) ? __builtin_amdgcn_readfirstlane(threadIdx.x >> 6)
-                                 : (int)(threadIdx.x >> 6);
+  // With 4 or 8 slots per lane (but FCFS) the wave's index in its block is
+  // taken into a scalar register: every row pointer derived from the instance
+  // is then scalar, which is what brings those kernels under 128 VGPRs (the
+  // narrower kernels ran slower with it, their scalar registers being the
+  // scarcer ones).
+  constexpr bool WIB_S = (K == 4 || K == 8) && POL != POL_FCFS;
+  const int wib = WIB_S ? __builtin_amdgcn_readfirstlane(threadIdx.x >> 6)
+                        : (int)(threadIdx.x >> 6);
   const int64_t inst = (int64_t)blockIdx.x * (blockDim.x >> 6) + wib;
   if (inst >= a.n_inst) return;
   const int lane = lane_id();
