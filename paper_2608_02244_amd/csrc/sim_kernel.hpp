@@ -721,7 +721,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
       while (relk < n) {
         if ((relk >> 6) != chunk) load_chunk(relk >> 6);
         const int off = relk & (WAVE - 1);
-        const uint64_t late = ballot(lane >= off && rel_t > t);
+        const uint64_t late = ballot((lane >= off) & (rel_t > t));
         const int hi = late ? __builtin_ctzll(late) : WAVE;
         if (POL != POL_FCFS && hi > off) {
           if (!any) {
@@ -784,7 +784,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
         int pre = wave_scan_incl(len + pp);            // reservations
         bool fit = (M == 0) || ((int64_t)(S.res + pre) <= M) ||
                    (S.nact == 0 && done == 0 && lane == 0);
-        uint64_t fm = ballot(lane < c && !fit);
+        uint64_t fm = ballot((lane < c) & !fit);
         int take = fm ? __builtin_ctzll(fm) : c;
         if (take > 0) {
           int base = 0;
@@ -863,7 +863,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
                 // reservation of gathered job j (prefill variant: + prompt)
                 const int rv = (PRE && j < G) ? glen[k] + P[pid(W[STG[j]])] : glen[k];
                 const int pre = wave_scan_incl(rv);
-                const uint64_t fm = ballot(j < G && j >= 1 && run + pre > M);
+                const uint64_t fm = ballot((j < G) & (j >= 1) & (run + pre > M));
                 if (fm) Bp = k * WAVE + __builtin_ctzll(fm);
                 else run += readlane(pre, 63);
               }
@@ -880,7 +880,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
             for (int k = 0; k < K; ++k) {
               if (k * WAVE < Bp && m == Bp) {
                 const int j = k * WAVE + lane;
-                const uint64_t fm = ballot(j < Bp && glen[k] <= alpha);
+                const uint64_t fm = ballot((j < Bp) & (glen[k] <= alpha));
                 if (fm) m = min(Bp, k * WAVE + __builtin_ctzll(fm));
               }
             }
@@ -1150,7 +1150,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
 #pragma unroll
           for (int k = 0; k < K; ++k)
             nie += __builtin_popcountll(
-                ballot(valid[k] && ws_end[k] == IDLE && (ws_q[k] & 0xFFFFu) == QNONE));
+                ballot(valid[k] & (ws_end[k] == IDLE) & ((ws_q[k] & 0xFFFFu) == QNONE)));
         }
         free_empty = nie;
         if (nie > 0) {
@@ -1217,7 +1217,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
         int ahead = 0;
 #pragma unroll
         for (int k = 0; k < K; ++k)
-          ahead += __builtin_popcountll(ballot(ws_end[k] != IDLE && (int64_t)ws_end[k] < lim0));
+          ahead += __builtin_popcountll(ballot((ws_end[k] != IDLE) & ((int64_t)ws_end[k] < lim0)));
         if (ahead >= 4) {
           const int N = S.nact;
           const int Gq = min(Qn, Beff);
@@ -1635,7 +1635,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
       if (S.min_end <= r_next) {
 #pragma unroll
         for (int k = 0; k < K; ++k)
-          quiet += __builtin_popcountll(ballot(ws_end[k] != IDLE && ws_end[k] <= r_next));
+          quiet += __builtin_popcountll(ballot((ws_end[k] != IDLE) & (ws_end[k] <= r_next)));
       }
     }
     // ISJL in FILL (or waiting on worker 1's timer) with A_max(t) > alpha: no
@@ -1954,7 +1954,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
           tn = min(tn, readlane(rel_t, __builtin_ctzll(mm)));
           break;
         }
-        if (ballot(lane >= off && rel_t >= tn)) break;  // the rest arrive after the span
+        if (ballot((lane >= off) & (rel_t >= tn))) break;  // the rest arrive after the span
         r = (r & ~(WAVE - 1)) + WAVE;
       }
     }

@@ -10,6 +10,8 @@ constexpr int WAVE = 64;
 
 __device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
 
+// Predicates of ballots are built with & rather than && when no operand reads
+// memory: the short-circuit form is compiled to lane-masked branches.
 __device__ __forceinline__ uint64_t ballot(bool p) { return (uint64_t)__ballot(p); }
 
 // Number of set bits of `mask` below the calling lane.
