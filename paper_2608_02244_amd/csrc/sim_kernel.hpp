@@ -583,8 +583,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       if (base < na) {
-        const bool el = valid[k] && ws_end[k] == IDLE &&
-                        (!need_empty_queue || (ws_q[k] & 0xFFFFu) == QNONE);
+        const bool el = valid[k] & (ws_end[k] == IDLE) &
+                        (!need_empty_queue | ((ws_q[k] & 0xFFFFu) == QNONE));
         const uint64_t bm = ballot(el);
         const int idx = base + mbcnt(bm);
         if (el && idx < na) {
@@ -1055,7 +1055,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
         for (int k = 0; k < K; ++k) {
           int w = k * WAVE + lane;
           uint32_t h = ws_q[k] & 0xFFFFu;
-          cand[k] = valid[k] && ws_end[k] == IDLE && h != QNONE && !(w == 0 && t < t_w1);
+          cand[k] = valid[k] & (ws_end[k] == IDLE) & (h != QNONE) & !((w == 0) & (t < t_w1));
           clen[k] = 0;  // reservation
           if (cand[k]) {
             const uint32_t wv = W[h];
