@@ -730,7 +730,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
             wave_lds_sync();
             any = true;
           }
-          if (lane >= off && lane < hi) atomicOr(&PEND[rel_r >> 5], 1u << (rel_r & 31));
+          if ((lane >= off) & (lane < hi)) atomicOr(&PEND[rel_r >> 5], 1u << (rel_r & 31));
           qcount += hi - off;
         }
         relk += hi - off;
@@ -791,7 +791,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
 #pragma unroll
           for (int k = 0; k < K; ++k) {
             if (base < take) {
-              bool idle = valid[k] && ws_end[k] == IDLE;
+              bool idle = valid[k] & (ws_end[k] == IDLE);
               uint64_t bm = ballot(idle);
               int idx = base + mbcnt(bm);
               int src = min(idx, WAVE - 1);
@@ -994,7 +994,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
               }
 #pragma unroll
               for (int k = 0; k < K; ++k)
-                if (k == (wsel >> 6) && lane == (wsel & 63)) {
+                if ((k == (wsel >> 6)) & (lane == (wsel & 63))) {
                   load[k] += len;
                   uint32_t h = ws_q[k] & 0xFFFFu;
                   if (h == QNONE) h = (uint32_t)r;
@@ -1300,7 +1300,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
               const int q = lane * K + k;
               const int e = de[k];
               const int e_nx = (k + 1 < K) ? de[k + 1 < K ? k + 1 : k] : e_up;
-              if (q < N && (q + 1 >= N || e_nx > e)) {
+              if ((q < N) & ((q + 1 >= N) | (e_nx > e))) {
                 if (q + 1 >= N || e + cg_max > alpha) lfail = q;
                 else if (M != 0 && alpha != IDLE && alpha + 1 - cg_max < e_nx) lcutq = q;
               }
@@ -1313,7 +1313,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
             for (int k = 0; k < K; ++k) {
               const int q = lane * K + k;
               const int e_nx = (k + 1 < K) ? de[k + 1 < K ? k + 1 : k] : e_up;
-              if (q < qf && e_nx > de[k]) lbelow++;
+              if ((q < qf) & (e_nx > de[k])) lbelow++;
             }
             go = wave_sum(lbelow) >= 3;
           }
@@ -1407,13 +1407,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
               const bool vq = q < N;
               const int e = de[k];
               const int e_nx = (k + 1 < K) ? de[k + 1 < K ? k + 1 : k] : e_up;
-              const bool ge = vq && (q + 1 >= N || e_nx > e);
+              const bool ge = vq & ((q + 1 >= N) | (e_nx > e));
               const int A = vq ? ap[k] : 0;
               const int pmA = at_job(pm, max(A - 1, 0));
               lim[k] = IDLE;
               if (ge) {
                 gem |= 1u << k;
-                bool ok = q + 1 < N && e < Hr && (A == 0 || pmA > e);
+                bool ok = (q + 1 < N) & (e < Hr) & ((A == 0) | (pmA > e));
                 if (POL == POL_ISJL) ok = ok && e + cg_max <= alpha;
                 if (!ok) {
                   lbad = q;
@@ -1435,7 +1435,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
 #pragma unroll
             for (int k = 0; k < K; ++k) {
               const int q = lane * K + k;
-              if (((gem >> k) & 1u) && q < pe && q <= pc) lpm = q;
+              if (((gem >> k) & 1u) & (q < pe) & (q <= pc)) lpm = q;
             }
             p_m = wave_max(lpm);
           }
@@ -1469,7 +1469,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
               const int e_nx = (k + 1 < K) ? de[k + 1 < K ? k + 1 : k] : e_up;
               const int A = vq ? ap[k] : 0;
               const int saA = at_job(sa, max(A - 1, 0)), sgA = at_job(sg, max(A - 1, 0));
-              if (((gem >> k) & 1u) && q <= p_m) {
+              if (((gem >> k) & 1u) & (q <= p_m)) {
                 const int Er = q == p_m ? tau_rel : e_nx;
                 const int64_t D = (int64_t)(Er - e);
                 const int64_t so = N - 1 - q, s = so + A;
@@ -1545,7 +1545,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
             int base = 0;
 #pragma unroll
             for (int k = 0; k < K; ++k) {
-              const bool idle = valid[k] && ws_end[k] == IDLE;
+              const bool idle = valid[k] & (ws_end[k] == IDLE);
               const uint64_t bm = ballot(idle);
               const int idx = base + mbcnt(bm);
               const int jc = min(idx, A_m - 1);
@@ -1765,8 +1765,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
             const bool valid = pos < N;
             const int e = t + (int)dk[k];
             const int e_next = (k + 1 < KS) ? t + (int)dk[k + 1 < KS ? k + 1 : k] : e_up;
-            const bool group_end = valid && (pos + 1 >= N || e_next > e);
-            if (group_end && (pos + 1 >= N || e - t + cg_max <= alpha)) lfound = pos;
+            const bool group_end = valid & ((pos + 1 >= N) | (e_next > e));
+            if (group_end & ((pos + 1 >= N) | (e - t + cg_max <= alpha))) lfound = pos;
             if (valid) cg_max = max(cg_max, dg[k]);
           }
           stop = min(stop, wave_min(lfound));
@@ -1782,7 +1782,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
             const bool valid = pos < N;
             const int e = t + (int)dk[k];
             const int e_next = (k + 1 < KS) ? t + (int)dk[k + 1 < KS ? k + 1 : k] : e_up;
-            if (valid && pos < stop && e_next > e) {
+            if (valid & (pos < stop) & (e_next > e)) {
               const int64_t D = (int64_t)(e_next - e);
               const int64_t s = N - 1 - pos;
               const int min_s = t - cg_max, max_s = t - cg_min;
@@ -1863,7 +1863,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
 #pragma unroll
           for (int k = 0; k < K; ++k) {
             const bool empty_q = (ws_q[k] & 0xFFFFu) == QNONE;
-            if (valid[k] && empty_q) {
+            if (valid[k] & empty_q) {
               if (ws_end[k] == IDLE) idle_empty = true;
               else fe = min(fe, ws_end[k]);
             }
@@ -1947,7 +1947,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
       while (r < n) {
         if ((r >> 6) != chunk) load_chunk(r >> 6);
         const int off = r & (WAVE - 1);
-        const bool in = lane >= off && rel_t < tn;
+        const bool in = (lane >= off) & (rel_t < tn);
         const bool m = in && rel_r < hr && S.res + (int64_t)plen(W[rel_r]) <= M;
         const uint64_t mm = ballot(m);
         if (mm) {
