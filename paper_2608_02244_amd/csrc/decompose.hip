@@ -286,8 +286,8 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
         lXm = max(lXm, ext);
         lAm = max(lAm, cnt_p);
         lP = max(lP, s * (uint32_t)t_next - sum_p);
-        if (Bcap > 0 && cnt_p > Bcap) lcap = true;
-        if (M != 0 && cnt_p >= 2 && (int64_t)res_p > M) lkv = true;
+        if ((Bcap > 0) & (cnt_p > Bcap)) lcap = true;
+        if ((M != 0) & (cnt_p >= 2) & ((int64_t)res_p > M)) lkv = true;
       }
     }
   };
@@ -307,8 +307,8 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
     const int pn = p + WAVE;
     nkey = pn < NE ? EV[pn] : 0xFFFFFFFFu;
     const int t = (int)(key >> 13);
-    const bool is_start = valid && ((key >> 12) & 1u);
-    const bool is_end = valid && !((key >> 12) & 1u);
+    const bool is_start = valid & (((key >> 12) & 1u) != 0u);
+    const bool is_end = valid & (((key >> 12) & 1u) == 0u);
     const int sj = is_start ? t : t - len;  // the job's start
     const int cnt_p = c_cnt + wave_scan_incl(is_start ? 1 : (is_end ? -1 : 0));
     // within a chunk the deltas sum to less than 64 x 2^20 in magnitude (times
@@ -323,7 +323,7 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
     const int t_first_next = (int)((uint32_t)readlane((int)nkey, 0) >> 13);
     if (lane == WAVE - 1) t_next = base + WAVE < NE ? t_first_next : t;
     const bool last = p == NE - 1;
-    const bool gend = valid && (last || t_next > t);
+    const bool gend = valid & (last | (t_next > t));
     // lane masks, each from one comparison (combined on the scalar unit)
     const int nv = NE - base;  // valid lanes: 0 .. nv - 1
     const uint64_t vmask = nv >= WAVE ? ~0ull : ((1ull << nv) - 1);
@@ -456,8 +456,8 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
                 }
               }
               if (found >= 0) {
-                cnt += __builtin_popcountll(ballot(ok && st_time == min_s));
-                if (ballot(ee >= 0 && ee <= gpos && st_time > min_s)) break;
+                cnt += __builtin_popcountll(ballot(ok & (st_time == min_s)));
+                if (ballot((ee >= 0) & (ee <= gpos) & (st_time > min_s))) break;
               }
               q += WAVE;
             }
@@ -486,8 +486,8 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
                 }
               }
               if (found >= 0) {
-                cnt += __builtin_popcountll(ballot(ok && st_time == max_s));
-                if (ballot(ee >= 0 && st_time < max_s)) break;
+                cnt += __builtin_popcountll(ballot(ok & (st_time == max_s)));
+                if (ballot((ee >= 0) & (st_time < max_s))) break;
               }
               q -= WAVE;
             }
@@ -535,7 +535,7 @@ __global__ __launch_bounds__(256) void decompose_kernel(DecArgs a) {
         gmax = c ? fmax : max0;
       }
     }
-    q_on = gend && !last;
+    q_on = gend & !last;
     q_t = t;
     q_tn = t_next;
     q_cnt = cnt_p;
