@@ -533,7 +533,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
       int pos = gbase + incl - cnt;
       uint32_t x = pool.w[i];
       const int base = (i * WAVE + lane) << 5;
-      while (x && pos < G) {
+      while ((x != 0u) & (pos < G)) {
         const int b = __builtin_ctz(x);
         x &= x - 1u;
         STG[pos] = (uint16_t)(base + b);
@@ -562,7 +562,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
           len = resv_len(pid(wv), plen(wv));
         }
         const int pre = wave_scan_incl(len);
-        const bool fail = j < G && (j > 0 || S.nact > 0) && (run + pre > M);
+        const bool fail = (j < G) & ((j > 0) | (S.nact > 0)) & (run + pre > M);
         const uint64_t fm = ballot(fail);
         if (fm) {
           const int f = __builtin_ctzll(fm);
@@ -587,7 +587,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
                         (!need_empty_queue | ((ws_q[k] & 0xFFFFu) == QNONE));
         const uint64_t bm = ballot(el);
         const int idx = base + mbcnt(bm);
-        if (el && idx < na) {
+        if (el & (idx < na)) {
           const uint32_t wv = W[STG[idx]];
           const int plan = plen(wv);
           const int len = true_len(pid(wv), plan);
@@ -782,8 +782,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
         int len = plen(wv), id = pid(wv);
         const int pp = (PRE && lane < c) ? P[id] : 0;  // prompt (prefill variant)
         int pre = wave_scan_incl(len + pp);            // reservations
-        bool fit = (M == 0) || ((int64_t)(S.res + pre) <= M) ||
-                   (S.nact == 0 && done == 0 && lane == 0);
+        bool fit = (M == 0) | ((int64_t)(S.res + pre) <= M) |
+                   ((S.nact == 0) & (done == 0) & (lane == 0));
         uint64_t fm = ballot((lane < c) & !fit);
         int take = fm ? __builtin_ctzll(fm) : c;
         if (take > 0) {
@@ -797,7 +797,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
               int src = min(idx, WAVE - 1);
               int l2 = __shfl(len, src), id2 = __shfl(id, src);
               const int p2 = PRE ? __shfl(pp, src) : 0;
-              if (idle && idx < take) {
+              if (idle & (idx < take)) {
                 ws_start[k] = t;
                 ws_end[k] = t + l2;
                 if (PRE) {
@@ -891,9 +891,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
             for (int k = 0; k < K; ++k) {
               int w = k * WAVE + lane;
               load[k] = 0;
-              if (w >= 1 && w < m) {
+              if ((w >= 1) & (w < m)) {
                 cap[k] = min(2 * alpha, o1 - glen[k] + beta);
-              } else if (w >= m && w < Bp) {
+              } else if ((w >= m) & (w < Bp)) {
                 cap[k] = alpha;
               } else {
                 cap[k] = -1;
@@ -1011,8 +1011,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
 #pragma unroll
             for (int k = 0; k < K; ++k) {
               int w = k * WAVE + lane;
-              if (w >= 1 && w < Bp) pmax = max(pmax, load[k]);
-              if (w >= 1 && w < m) {
+              if ((w >= 1) & (w < Bp)) pmax = max(pmax, load[k]);
+              if ((w >= 1) & (w < m)) {
                 uint32_t r = STG[w];
                 uint32_t h = ws_q[k] & 0xFFFFu, tl = ws_q[k] >> 16;
                 if (tl != QNONE) qn_set((int)tl, r);
@@ -1301,8 +1301,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
               const int e = de[k];
               const int e_nx = (k + 1 < K) ? de[k + 1 < K ? k + 1 : k] : e_up;
               if ((q < N) & ((q + 1 >= N) | (e_nx > e))) {
-                if (q + 1 >= N || e + cg_max > alpha) lfail = q;
-                else if (M != 0 && alpha != IDLE && alpha + 1 - cg_max < e_nx) lcutq = q;
+                if ((q + 1 >= N) | (e + cg_max > alpha)) lfail = q;
+                else if ((M != 0) & (alpha != IDLE) & (alpha + 1 - cg_max < e_nx)) lcutq = q;
               }
               if (q < N) cg_max = max(cg_max, dg[k]);
             }
@@ -1356,7 +1356,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
 #pragma unroll
                 for (int step = NS; step >= 1; step >>= 1) {
                   const int x = at_job(pq, min(lo + step, NS) - 1);
-                  if (lo + step <= NS && x <= bb) lo += step;
+                  if ((lo + step <= NS) & (x <= bb)) lo += step;
                 }
                 v = min(v, lo);
               }
@@ -1374,7 +1374,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
 #pragma unroll
             for (int step = NS; step >= 1; step >>= 1) {
               const int x = at_pos(ap, min(lo + step, NS) - 1);
-              if (lo + step <= NS && x <= j) lo += step;
+              if ((lo + step <= NS) & (x <= j)) lo += step;
             }
             const int e = at_pos(de, min(lo, NS - 1));
             sg[k] = lo < N ? e : IDLE;
@@ -1550,7 +1550,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
               const int idx = base + mbcnt(bm);
               const int jc = min(idx, A_m - 1);
               const int s_rel = at_job(sg, jc), L = at_job(qlen, jc);
-              if (idle && idx < A_m) {
+              if (idle & (idx < A_m)) {
                 const int rk = POL == POL_FCFS ? head + idx : (int)STG[idx];
                 const int st = t + s_rel;
                 emit(pid(W[rk]), st, L);
