@@ -39,6 +39,9 @@ def kernel_sources_sha256() -> str:
     for f in KERNEL_SOURCES:
         with open(os.path.join(ROOT, "paper_2608_02244_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
+    # the compiler flags are part of what the counters measured
+    with open(os.path.join(ROOT, "paper_2608_02244_amd", "buildlib.py"), "rb") as fh:
+        h.update(fh.read())
     return h.hexdigest()
 
 
