@@ -23,10 +23,21 @@ ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           f"-I{INCLUDE}", f"-I{CSRC}"]
-# The simulation kernels (csrc/sim_*.hip) are scheduled by LLVM's iterative
-# max-occupancy strategy, measured faster on their event loops; the re-scoring
-# kernel ran slower with it, and the other sources keep the default scheduler.
+# Instruction scheduling strategies, chosen by measurement: the simulation
+# kernels (csrc/sim_*.hip) by LLVM's iterative max-occupancy strategy, the
+# re-scoring kernel by max-ILP (with the other's strategy each ran slower); the
+# other sources keep the default.
 SIM_FLAGS = ["-mllvm", "-amdgpu-sched-strategy=iterative-maxocc"]
+DEC_FLAGS = ["-mllvm", "-amdgpu-sched-strategy=max-ilp"]
+
+
+def _flags(src: str) -> list:
+    name = os.path.basename(src)
+    if name.startswith("sim_"):
+        return SIM_FLAGS
+    if name == "decompose.hip":
+        return DEC_FLAGS
+    return []
 
 
 def _hipcc() -> str:
@@ -39,8 +50,7 @@ def _hipcc() -> str:
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    extra = SIM_FLAGS if os.path.basename(src).startswith("sim_") else []
-    cmd = [_hipcc()] + COMMON + extra + lang + ["-c", src, "-o", obj]
+    cmd = [_hipcc()] + COMMON + _flags(src) + lang + ["-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
