@@ -171,7 +171,8 @@ struct SimState {
 // scratch (else in LDS).  Every kernel with up to 8 slots per lane but FCFS's
 // is held to 128 VGPRs, so that 4 waves share a SIMD where the LDS allows 16
 // per CU (FCFS's 4- and 8-slot kernels ran slower that way and keep 3).
-template <int POL, int K, int NW, bool GEN, bool ROB, bool PRE, bool FILL, bool QH = false>
+template <int POL, int K, int NW, bool GEN, bool ROB, bool PRE, bool FILL, bool QH = false,
+          bool FAIR = false>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <= 2 || (K <= 8 && POL != POL_FCFS) ? 4 : (K <= 8 ? 3 : 1)))) void simulate_kernel(SimArgs a) {
   static_assert(!ROB || POL == POL_ISJL, "predicted sizes: ISJL only");
   static_assert(!FILL || (K <= 2 && !ROB && !PRE && POL != POL_LJF), "fill sweep variants");
@@ -654,8 +655,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
     return admit_prefix(t, G, need_empty_queue, adm, adm_len, adm_minlen);
   };
 
+  // FAIR: launched when every wave of the grid is resident at once, so that the
+  // launch lasts as long as its slowest wave.  A SIMD's arbiter issues for its
+  // oldest wave first, which leaves the youngest to finish alone, one
+  // dependent instruction at a time; turning each wave's priority with its
+  // event count shares the issue slots among the SIMD's waves instead.
+  int fair_turn = FAIR ? __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)) : 0;
   while (true) {
     const int t = S.t;
+    if constexpr (FAIR) {
+      switch (fair_turn++ & 3) {
+        case 0: __builtin_amdgcn_s_setprio(0); break;
+        case 1: __builtin_amdgcn_s_setprio(1); break;
+        case 2: __builtin_amdgcn_s_setprio(2); break;
+        default: __builtin_amdgcn_s_setprio(3); break;
+      }
+    }
     // (1) retire the jobs whose last token was processed at t-1
     if (S.min_end == t) {
       // the earliest / latest start is searched again only if a job holding
@@ -2045,6 +2060,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
   }
 }
 
+// Whether a grid of `blocks` blocks of `wpb` waves fits the device at once
+// (every block resident from the start); false when the runtime cannot tell.
+inline bool resident_at_once(const void* kern, int64_t blocks, int wpb, size_t lds) {
+  int per_cu = 0, dev = 0, n_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, wpb * WAVE, lds) != hipSuccess ||
+      hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return blocks <= (int64_t)per_cu * n_cu;
+}
+
 // The fill sweep serves FCFS and SJF with up to 2 slots per lane, and ISJL there
 // when alpha is at least the length limit (A_max, below every length, never
 // exceeds it).  With a finite budget ISJL's completions mostly meet the guard
@@ -2063,6 +2091,14 @@ hipError_t launch_sim(const SimArgs& a, int K, int NW, bool general, int wpb, si
   const bool qh = POL == POL_ISJL && K <= 8 && !fill && a.qlink != nullptr;
 #define FS_LAUNCH(KK, NN, GG, FF, QQ)                                                     \
   if (K == KK && NW == NN && general == GG && fill == FF && qh == QQ) {                   \
+    if constexpr (!GG && KK <= 8) {                                                       \
+      if (resident_at_once((const void*)simulate_kernel<POL, KK, NN, GG, ROB, PRE, FF, QQ, true>, \
+                           blocks, wpb, lds)) {                                           \
+        hipLaunchKernelGGL((simulate_kernel<POL, KK, NN, GG, ROB, PRE, FF, QQ, true>), grid, block, \
+                           lds, s, a);                                                    \
+        return hipGetLastError();                                                         \
+      }                                                                                   \
+    }                                                                                     \
     hipLaunchKernelGGL((simulate_kernel<POL, KK, NN, GG, ROB, PRE, FF, QQ>), grid, block, lds, \
                        s, a);                                                             \
     return hipGetLastError();                                                             \

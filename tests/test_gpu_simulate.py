@@ -467,6 +467,28 @@ def test_plan_links_in_hbm(dev, alpha):
                     fi.cpu().numpy(), rf)
 
 
+@pytest.mark.parametrize("policy,alpha", [("fcfs", ALPHA_INF), ("sjf", ALPHA_INF), ("ljf", 4),
+                                          ("isjl", 40), ("isjl", ALPHA_INF)])
+def test_one_round_and_many_round_launches(dev, policy, alpha):
+    """A grid whose waves are all resident at once takes the kernels that turn
+    each wave's issue priority with its event count; a larger grid the kernels
+    without.  On the same instances both give the same metrics and schedules
+    (1, 2, 4 and 8 slots per lane; sorted, unsorted and no releases), and the
+    first instances match the oracle."""
+    rng = np.random.default_rng(zlib.crc32(f"rounds:{policy}:{alpha}".encode()))
+    for B, arr in ((50, 400), (128, -300), (200, 300), (300, 0)):
+        a, p, o = workload.random_tables(rng, 12288, 300, 40, 120, max_arrival=abs(arr),
+                                         sorted_arrivals=arr > 0)
+        kw = dict(policy=policy, B=B, alpha=alpha, M_kv=6000, cost_c=3, cost_tau=1)
+        ctx = f"one round vs many policy={policy} alpha={alpha} B={B} arrivals={arr}"
+        log(ctx)
+        big, bs, bf = gpu_sim(dev, a, p, o, **kw)
+        small, ss, sf = gpu_sim(dev, a[:256], p[:256], o[:256], **kw)
+        assert_same(ctx, small, big[:256], ss, bs[:256], sf, bf[:256])
+        ref, rs, rf = oracle.simulate(a[:6], p[:6], o[:6], schedule=True, **kw)
+        assert_same(ctx + " oracle", small[:6], ref, ss[:6], rs, sf[:6], rf)
+
+
 @pytest.mark.parametrize("policy,alpha", [("fcfs", ALPHA_INF), ("sjf", ALPHA_INF),
                                           ("isjl", 25), ("isjl", 300), ("isjl", ALPHA_INF)])
 def test_releases_behind_a_blocked_head(dev, policy, alpha):
