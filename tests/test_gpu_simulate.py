@@ -489,6 +489,47 @@ def test_one_round_and_many_round_launches(dev, policy, alpha):
         assert_same(ctx + " oracle", small[:6], ref, ss[:6], rs, sf[:6], rf)
 
 
+@pytest.mark.parametrize("variant", ["prefill", "robust", "robust_prefill"])
+def test_one_round_and_many_round_launches_variants(dev, variant):
+    """The prefill and predicted-size variants of ISJL (alpha = 40) take the
+    turning-priority kernels in a grid resident at once too: the same
+    instances in a one-round and a many-round launch give the same metrics and
+    schedules, and the first instances match the oracle."""
+    import torch
+    rng = np.random.default_rng(zlib.crc32(f"rounds:{variant}".encode()))
+    pre = variant.endswith("prefill")
+    rob = variant.startswith("robust")
+    for B, arr in ((50, 400), (128, -300), (300, 0)):
+        a, p, o = workload.random_tables(rng, 12288, 300, 40, 120, max_arrival=abs(arr),
+                                         sorted_arrivals=arr > 0)
+        u = workload.prediction_upper(o, 0.5, seed=B)
+        kw = dict(B=B, alpha=40, M_kv=6000, cost_c=3, cost_tau=1)
+        ctx = f"one round vs many {variant} B={B} arrivals={arr}"
+        log(ctx)
+
+        def run(k):
+            tabs = (a[:k], p[:k], o[:k]) + ((u[:k],) if rob else ())
+            ts = [torch.from_numpy(np.ascontiguousarray(x)).to(dev) for x in tabs]
+            if rob:
+                raw, st, fi = fs.simulate_robust(*ts, prefill=pre, schedule=True, **kw)
+            else:
+                raw, st, fi = fs.simulate(*ts, policy="isjl", prefill=pre, schedule=True, **kw)
+            torch.cuda.synchronize()
+            return fs.metrics_view(raw), st.cpu().numpy(), fi.cpu().numpy()
+
+        big, bs, bf = run(12288)
+        small, ss, sf = run(256)
+        assert_same(ctx, small, big[:256], ss, bs[:256], sf, bf[:256])
+        flags = oracle.FLAG_PREFILL if pre else 0
+        if rob:
+            ref, rs, rf = oracle.simulate_robust(a[:4], p[:4], o[:4], u[:4], schedule=True,
+                                                 flags=flags, **kw)
+        else:
+            ref, rs, rf = oracle.simulate(a[:4], p[:4], o[:4], policy="isjl", schedule=True,
+                                          flags=flags, **kw)
+        assert_same(ctx + " oracle", small[:4], ref, ss[:4], rs, sf[:4], rf)
+
+
 @pytest.mark.parametrize("policy,alpha", [("fcfs", ALPHA_INF), ("sjf", ALPHA_INF),
                                           ("isjl", 25), ("isjl", 300), ("isjl", ALPHA_INF)])
 def test_releases_behind_a_blocked_head(dev, policy, alpha):
