@@ -108,23 +108,6 @@ struct PoolBits {
     }
     return -1;
   }
-  // first set rank >= r0, -1 if none
-  __device__ __forceinline__ int first_from(int r0, int lane) const {
-#pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      int base = (i * WAVE + lane) << 5;
-      uint32_t x = w[i];
-      if (base + 32 <= r0) x = 0u;
-      else if (base < r0) x &= ~((1u << (r0 - base)) - 1u);
-      uint64_t m = ballot(x != 0u);
-      if (m) {
-        int L = __builtin_ctzll(m);
-        uint32_t y = (uint32_t)readlane((int)x, L);
-        return ((i * WAVE + L) << 5) + __builtin_ctz(y);
-      }
-    }
-    return -1;
-  }
   __device__ __forceinline__ void reset(int r, int lane) {
     int L = (r >> 5) & (WAVE - 1), wi = r >> 11;
     uint32_t b = 1u << (r & 31);
@@ -922,7 +905,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
             // Pack scan (Algorithm 3): remaining queued jobs in decreasing length;
             // each goes to the first spare worker with room, else to the long
             // worker of largest index with room; a job that fits nowhere stays.
-            int cur = rlast;
             const bool has_spare = uni(Bp) > m;
             // Each worker choice below is one ballot per slot register, built
             // from plain comparisons (no short-circuit, which the compiler
@@ -939,9 +921,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
                 long_m[k] = ballot((w >= 1) & (w < m));
               }
             }
+            // the ranks still to visit: the queued ranks after rlast (pool was
+            // cleared up to it), each cleared once visited
+            PoolBits<NW> scan = pool;
             while (true) {
-              const int r = pool.first_from(cur + 1, lane);
+              const int r = scan.first();
               if (r < 0) break;
+              scan.reset(r, lane);
               const int len = plen(W[r]);
               int wsel = -1;
               if (has_spare) {  // spare workers, ascending
@@ -994,7 +980,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
                 const uint64_t fm2 = ballot(q < hi && plen(W[q]) <= remmax);
                 const int b = fm2 ? lo + __builtin_ctzll(fm2) : hi;
                 if (b >= n) break;
-                cur = b - 1;
+                scan.clear_upto(b - 1, lane);
                 continue;
               }
               // append r to worker wsel's queue
@@ -1018,7 +1004,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
               pool.reset(r, lane);
               --qcount;
               planned++;
-              cur = r;
             }
             wave_lds_sync();
             // worker j in 2..M: its pack, then o_j; worker 1: o_1
