@@ -1050,6 +1050,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
       if (planned > 0 && amax <= alpha) {
         bool cand[K];
         int clen[K];
+        uint32_t cwv[K];
         int csum = 0, ccnt = 0;
 #pragma unroll
         for (int k = 0; k < K; ++k) {
@@ -1057,8 +1058,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
           uint32_t h = ws_q[k] & 0xFFFFu;
           cand[k] = valid[k] & (ws_end[k] == IDLE) & (h != QNONE) & !((w == 0) & (t < t_w1));
           clen[k] = 0;  // reservation
+          cwv[k] = 0u;
           if (cand[k]) {
             const uint32_t wv = W[h];
+            cwv[k] = wv;
             clen[k] = resv_len(pid(wv), plen(wv));
           }
           csum += clen[k];
@@ -1097,7 +1100,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FILL || K <
           for (int k = 0; k < K; ++k) {
             if (cand[k]) {
               uint32_t h = ws_q[k] & 0xFFFFu;
-              uint32_t wv = W[h];
+              const uint32_t wv = cwv[k];
               const int plan = plen(wv);
               const int len = true_len(pid(wv), plan);
               ws_start[k] = t;
